@@ -1,0 +1,181 @@
+"""Budget-exact cached sampling, Alg. 2 with the Eq. 3 state (oracle).
+
+TEST INFRASTRUCTURE ONLY -- see the package docstring.
+
+One sample of T Euler flow-matching steps.  At step t:
+
+ 1. m_t = S(LN(h_t)(1 + scale0_t) + shift0_t), h_t = S(S(x_t) W_in^T + b_in):
+    the first block's modulated image-token input of the conditional branch
+    (``indicator="patch"`` uses h_t itself, the paper's post-patch-embedding
+    tensor of Eq. 3).
+ 2. t = 0 computes (m_0 = 1, Sec. 3.1).  Otherwise the state of Eq. 3 is
+    formed with relative-L1 norms (sums in float64) and the gate decides;
+    the two budget rules of Alg. 2 then override it: spend the remainder
+    when B - c >= T - t, reuse when B - c = 0.
+ 3. Compute: run the block stack per branch, refresh r = S(h_out - h);
+    reuse: h_out = S(h + r) (plain residual reuse, Sec. 3.1 / App. A.1).
+ 4. v from the final layer; guidance v = v_u + g (v_c - v_u) with one shared
+    decision for both branches (App. A.1).
+ 5. x_{t+1} = f32(x_t + dsigma_t v), dsigma_t = f32(sigma_{t+1} - sigma_t).
+
+State vector (8 features; gates with d_0 = 6 read the first six, which are
+exactly Eq. 3's s_bud and s_traj):
+  f0 = B/T, f1 = (B-c)/B, f2 = (B-c)/(T-t), f3 = t - t_last,
+  f4 = |m_t - m_last|_1 / |m_last|_1, f5 = |m_t - m_{t-1}|_1 / |m_{t-1}|_1,
+  f6 = t/T (step fraction), f7 = sum of f5 since the last computed step.
+c = computed steps before t; denominators are max(sum, 1e-30).
+"""
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import dit
+from .gate import parse_gate_blob, tau_logit
+from .numerics import round_f32, storage_to_f64
+
+N_FEATURES = 8
+DENOM_FLOOR = 1e-30
+
+
+def sigma_schedule(T: int, shift: float = 1.0):
+    """sigma_i = s u / (1 + (s - 1) u), u = 1 - i/T, i = 0..T (float64)."""
+    u = 1.0 - np.arange(T + 1, dtype=np.float64) / T
+    return shift * u / (1.0 + (shift - 1.0) * u)
+
+
+def budget_features(B, T, t, c):
+    """s_bud of Eq. 3: target ratio, remaining fraction, remaining pressure."""
+    return [B / T, (B - c) / B, (B - c) / (T - t)]
+
+
+def decide(z, B, T, t, c, tau=0.5):
+    """Alg. 2 decision at step t >= 1 with c computed steps so far.
+
+    Returns (m_t, forced).  The gate's vote is z > logit(tau) (strict; a NaN
+    logit votes reuse); 'spend remainder' then forces 1 when B - c >= T - t,
+    'budget exhausted' forces 0 when B - c = 0."""
+    m = 1 if (z > tau_logit(tau)) else 0
+    forced = 0
+    if B - c >= T - t:
+        m, forced = 1, 1
+    if B - c == 0:
+        m, forced = 0, 1
+    return m, forced
+
+
+def rel_l1_sums(a, b):
+    """(sum |a - b|, sum |b|) in float64."""
+    return float(np.abs(a - b).sum()), float(np.abs(b).sum())
+
+
+@dataclass
+class SampleResult:
+    x: np.ndarray                     # final latent, float32 values [N, C]
+    full: np.ndarray                  # uint8 [T]
+    logit: np.ndarray                 # float64 [T], NaN at t = 0
+    forced: np.ndarray                # uint8 [T]
+    features: np.ndarray              # float64 [T, 8], NaN row at t = 0
+    sums: np.ndarray                  # float64 [T, 4]: |m-m_prev|, |m_prev|, |m-m_last|, |m_last|
+    nfe: int
+    trace: dict = field(default_factory=dict)
+
+
+def sample(cfg, weights, gate_blob, x0, text, T, B, *, sigmas=None, shift=1.0,
+           tau=0.5, guidance=1.0, forced_mask=None, indicator="modulated",
+           trace=False, gate_fn=None):
+    """Run one cached sample.
+
+    cfg       model config (attributes as in the workload registry)
+    weights   dict name -> storage array (uint16 bf16 bits or float32)
+    gate_blob float32 gate blob (ignored if ``gate_fn`` is given)
+    x0        float32 [N, C]; text: storage [batch, N_t, ctx]
+    forced_mask optional uint8 [T]: replaces every decision (replay)
+    gate_fn   optional callable(features) -> logit, for tests
+    """
+    if not (1 <= B <= T):
+        raise ValueError("budget must satisfy 1 <= B <= T")
+    P = dit.Params(cfg, weights)
+    rs = P.rs
+    gate = None if gate_fn is not None else parse_gate_blob(gate_blob)
+    logit_fn = gate_fn if gate_fn is not None else gate.logit
+    if sigmas is None:
+        sigmas = sigma_schedule(T, shift)
+    sigmas = np.asarray(sigmas, np.float64)
+    assert sigmas.shape == (T + 1,)
+    if forced_mask is not None:
+        forced_mask = np.asarray(forced_mask, np.uint8)
+        if forced_mask.shape != (T,) or forced_mask[0] != 1 or int(forced_mask.sum()) != B:
+            raise ValueError("forced mask must have m_0 = 1 and exactly B ones")
+
+    nb = cfg.batch
+    text64 = [storage_to_f64(text[b], cfg.dtype) for b in range(nb)]
+    txt = [dit.text_in(P, text64[b]) for b in range(nb)]
+    mods = [dit.mod_table(P, dit.vec_table(P, sigmas[:T], text64[b])) for b in range(nb)]
+
+    x = round_f32(np.asarray(x0, np.float64))
+    full = np.zeros(T, np.uint8)
+    forced = np.zeros(T, np.uint8)
+    logit = np.full(T, np.nan)
+    feats = np.full((T, N_FEATURES), np.nan)
+    sums = np.full((T, 4), np.nan)
+    r = [None] * nb
+    c = 0
+    t_last = 0
+    acc = 0.0
+    m_prev = m_last = None
+    tr = {"m": [], "h": [], "r": [], "v": []} if trace else {}
+
+    for t in range(T):
+        h = dit.patch_embed(P, x)
+        if indicator == "patch":
+            m_t = h
+        else:
+            sh0, sc0 = dit.first_block_shift_scale(P, mods[0][t])
+            m_t = rs(dit.modulate(h, sh0, sc0))
+        if t == 0:
+            dec, frc = 1, 1
+        else:
+            s_p = rel_l1_sums(m_t, m_prev)
+            s_l = rel_l1_sums(m_t, m_last)
+            sums[t] = [s_p[0], s_p[1], s_l[0], s_l[1]]
+            d_prev = s_p[0] / max(s_p[1], DENOM_FLOOR)
+            d_last = s_l[0] / max(s_l[1], DENOM_FLOOR)
+            acc += d_prev
+            f = budget_features(B, T, t, c) + [float(t - t_last), d_last, d_prev, t / T, acc]
+            feats[t] = f
+            z = logit_fn(np.asarray(f))
+            logit[t] = z
+            dec, frc = decide(z, B, T, t, c, tau)
+            if forced_mask is not None:
+                dec = int(forced_mask[t])
+        full[t], forced[t] = dec, frc
+
+        v_b = []
+        for b in range(nb):
+            if dec:
+                h_out = dit.block_stack(P, h, txt[b], mods[b][t])
+                r[b] = rs(h_out - h)
+            else:
+                h_out = rs(h + r[b])
+            v_b.append(dit.final_layer(P, h_out, mods[b][t]))
+        if dec:
+            c += 1
+            t_last = t
+            m_last = m_t
+            acc = 0.0
+        v = v_b[0] if nb == 1 else v_b[1] + guidance * (v_b[0] - v_b[1])
+        dsig = float(np.float32(sigmas[t + 1] - sigmas[t]))
+        x = round_f32(x + dsig * v)
+        m_prev = m_t
+        if t == 0:
+            m_last = m_t
+        if trace:
+            tr["m"].append(m_t)
+            tr["h"].append(h)
+            tr["r"].append([None if rb is None else rb.copy() for rb in r])
+            tr["v"].append(v)
+
+    if c != B:
+        raise AssertionError(f"realised NFE {c} != budget {B}")
+    return SampleResult(x=x, full=full, logit=logit, forced=forced, features=feats,
+                        sums=sums, nfe=c, trace=tr)
