@@ -1,0 +1,970 @@
+// Host driver and C ABI of the budget-aware cached DiT sampler.
+//
+// Per sample: text projection, timestep/pooled embeddings and the whole
+// modulation table (all steps) run once.  Per step t: patch embed + the
+// indicator kernel (modulated first-block input and its relative-L1
+// partial sums) + a fixed-order reduction written straight into pinned
+// host memory; the host waits for that one event, evaluates the gate
+// (Eq. 1) on the 8-feature state and applies Alg. 2's budget rules in
+// double precision; then it enqueues either the full block stack (with
+// the residual refresh) or the residual reuse, and the final layer with
+// the Euler update.  Every tensor operation is a HIP kernel.
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <type_traits>
+#include <vector>
+
+#include "../../include/dit_cache.h"
+#include "../../include/dit_kernels.h"
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_create_error;
+
+struct Lin {
+  const void* w = nullptr;
+  const void* b = nullptr;
+  int out = 0, in = 0;
+};
+struct DoubleW { Lin qkv[2], o[2], mlp0[2], mlp1[2]; };  // [0] image, [1] text stream
+struct SingleW { Lin l1, l2; };
+struct CrossW { const void* mod_off = nullptr; Lin qkv, o, xq, xkv, xo, ffn0, ffn1; };
+
+struct Model {
+  Lin img_in, txt_in, time0, time2, pool0, pool2, mod, fin;
+  std::vector<DoubleW> dbl;
+  std::vector<SingleW> sgl;
+  std::vector<CrossW> crs;
+};
+
+struct GateMLP {
+  std::vector<int> widths;
+  bool z = false;
+  std::vector<double> mu, sd;
+  std::vector<std::vector<double>> W, b;
+};
+
+struct Pending {
+  int cls;
+  double work;
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct dit_cache {
+  dit_model_config cfg{};
+  hipStream_t stream = nullptr;
+  int n_cu = 256;
+  bool bf16 = true;
+  size_t esz = 2;
+  int H = 0, F = 0, N = 0, Nt = 0, L = 0, C = 0, nb = 1, n_mod = 0, ldY = 0;
+
+  void* wdev = nullptr;
+  size_t wbytes = 0;
+  Model M;
+
+  // workspace (storage dtype unless noted)
+  void* xs = nullptr;      // [N, C]
+  void* h = nullptr;       // [N, H]
+  void* mbuf[3] = {};      // [N, H] indicator tensors (rotating)
+  void* r = nullptr;       // [nb, N, H] cached residual per branch
+  void* X = nullptr;       // [L, H] joint hidden state
+  void* A = nullptr;       // [L, H] modulated block input
+  void* Y = nullptr;       // [L, 4H+F]: q | k | v | attn out | mlp hidden
+  void* vt = nullptr;      // bf16 [heads, 128, round_up(L, 64)]
+  void* hout = nullptr;    // [N, H]
+  void* yf = nullptr;      // [N, H] final-layer input
+  float* vel = nullptr;    // f32 [nb, N, C]
+  void* txt = nullptr;     // [nb, Nt, H]
+  void* ctxkv = nullptr;   // [Nt, 2H] cross-attention k | v
+  void* vt2 = nullptr;     // bf16 [heads, 128, round_up(Nt, 64)]
+  float* ones = nullptr;   // f32 [H] (ungated residual)
+  double* partials = nullptr;
+  int max_partials = 0;
+  double* sums_host = nullptr;  // pinned, mapped [4]
+  double* sums_dev = nullptr;
+  hipEvent_t ev_sums = nullptr;
+
+  // per-sample buffers, grown on demand (sized by T)
+  int cap_T = 0;
+  float* mod = nullptr;    // f32 [nb, T, n_mod]
+  float* modx = nullptr;   // f32 [nb, n_cross, T, 6H]
+  void* temb = nullptr;    // [T, time_dim]
+  void* th = nullptr;      // [T, H]
+  float* tv = nullptr;     // f32 [T, H]
+  void* pooled = nullptr;  // [1, ctx]
+  void* ph = nullptr;      // [1, H]
+  float* pv = nullptr;     // f32 [1, H]
+  void* svec = nullptr;    // [T, H]
+  double* sig_dev = nullptr;
+
+  std::string err;
+
+  bool prof = false;
+  dit_stats stats{};
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  std::vector<Pending> pending;
+};
+
+namespace {
+
+using dit::GemmArgs;
+
+dit_status fail(dit_cache* c, dit_status s, const std::string& msg) {
+  if (c) c->err = msg; else g_create_error = msg;
+  return s;
+}
+
+#define HIPCK(expr)                                                                    \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(c, DIT_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_));     \
+  } while (0)
+
+#define TRY(expr)                          \
+  do {                                     \
+    dit_status s_ = (expr);                \
+    if (s_ != DIT_OK) return s_;           \
+  } while (0)
+
+inline size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------- profiling
+hipEvent_t next_event(dit_cache* c) {
+  if (c->ev_used == c->ev_pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->ev_pool.push_back(e);
+  }
+  return c->ev_pool[c->ev_used++];
+}
+
+struct Scope {
+  dit_cache* c;
+  int cls;
+  double work;
+  hipEvent_t a = nullptr;
+  Scope(dit_cache* c_, int cls_, double work_) : c(c_), cls(cls_), work(work_) {
+    if (c->prof) {
+      a = next_event(c);
+      if (a) hipEventRecord(a, c->stream);
+    }
+  }
+  ~Scope() {
+    if (c->prof && a) {
+      hipEvent_t b = next_event(c);
+      if (b) {
+        hipEventRecord(b, c->stream);
+        c->pending.push_back({cls, work, a, b});
+      }
+    }
+  }
+};
+
+void collect_events(dit_cache* c) {
+  if (!c->prof) return;
+  hipStreamSynchronize(c->stream);
+  for (const Pending& p : c->pending) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+      c->stats.ms[p.cls] += ms;
+      c->stats.work[p.cls] += p.work;
+      c->stats.launches[p.cls] += 1;
+    }
+  }
+  c->pending.clear();
+  c->ev_used = 0;
+}
+
+// ---------------------------------------------------------------- helpers
+const char* sp(const dit_cache* c, const void* base, size_t elem_off) {
+  return (const char*)base + elem_off * c->esz;
+}
+char* sp(const dit_cache* c, void* base, size_t elem_off) { return (char*)base + elem_off * c->esz; }
+
+GemmArgs lin_args(const dit_cache* c, const void* A, int64_t lda, const Lin& l, void* C, int64_t ldc,
+                  int M, int flags = DIT_EPI_STORE) {
+  GemmArgs g{};
+  g.A = A; g.lda = lda; g.W = l.w; g.ldw = l.in; g.bias = l.b;
+  g.C = C; g.ldc = ldc; g.gate = nullptr;
+  g.M = M; g.N = l.out; g.K = l.in; g.flags = flags;
+  return g;
+}
+
+dit_status gemm(dit_cache* c, GemmArgs* g, int n, int cls) {
+  double flops = 0;
+  for (int i = 0; i < n; ++i) flops += 2.0 * g[i].M * (double)g[i].N * g[i].K;
+  Scope sc(c, cls, flops);
+  if (c->bf16) {
+    HIPCK(dit::launch_gemm_bf16(g, n, c->stream, c->n_cu));
+  } else {
+    HIPCK(dit::launch_gemm_f32(g, n, c->stream));
+    for (int i = 0; i < n; ++i)
+      if (g[i].rms_cols > 0)
+        HIPCK(dit::launch_rms_heads_f32((float*)g[i].C, g[i].ldc, g[i].M, g[i].rms_cols,
+                                        c->cfg.head_dim, c->stream));
+  }
+  return DIT_OK;
+}
+
+template <typename Fn>
+dit_status typed(dit_cache* c, Fn fn) {
+  hipError_t e = c->bf16 ? fn((bf16_t*)nullptr) : fn((float*)nullptr);
+  if (e != hipSuccess) return fail(c, DIT_EHIP, std::string("kernel launch: ") + hipGetErrorString(e));
+  return DIT_OK;
+}
+
+dit_status ln_mod(dit_cache* c, const void* x, int64_t ldx, void* out, int64_t ldo, int rows, int split,
+                  const float* sh0, const float* sc0, const float* sh1, const float* sc1, int cls) {
+  Scope s(c, cls, 2.0 * rows * c->H * c->esz);
+  return typed(c, [&](auto* tp) {
+    using T = std::remove_pointer_t<decltype(tp)>;
+    return dit::launch_ln_mod<T>((const T*)x, ldx, (T*)out, ldo, rows, c->H, split, sh0, sc0, sh1, sc1,
+                                 c->stream);
+  });
+}
+
+// attention over joint rows: q,k,v inside Y (or separate), output into o
+dit_status attention(dit_cache* c, const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v,
+                     int64_t ldv, void* o, int64_t ldo, int Lq, int Lk, void* vt_ws) {
+  const int heads = c->cfg.heads, hd = c->cfg.head_dim;
+  const double flops = 4.0 * Lq * (double)Lk * heads * hd;
+  if (c->bf16) {
+    {
+      Scope s(c, DIT_K_FULL_OTHER, 2.0 * Lk * heads * hd * 2);
+      HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt_ws, Lk, heads, c->stream));
+    }
+    Scope s(c, DIT_K_ATTN, flops);
+    HIPCK(dit::launch_flash_attn_bf16(q, ldq, k, ldk, vt_ws, (int)rup(Lk, 64), o, ldo, Lq, Lk, heads,
+                                      c->stream));
+  } else {
+    Scope s(c, DIT_K_ATTN, flops);
+    HIPCK(dit::launch_attn_f32((const float*)q, ldq, (const float*)k, ldk, (const float*)v, ldv,
+                               (float*)o, ldo, Lq, Lk, heads, hd, c->stream));
+  }
+  return DIT_OK;
+}
+
+// ---------------------------------------------------------------- weights
+dit_status layout(dit_cache* c, size_t* total_elems) {
+  const dit_model_config& g = c->cfg;
+  const int H = g.hidden, F = g.mlp_hidden, C = g.in_channels, X = g.ctx_dim;
+  size_t off = 0;
+  auto take = [&](Lin& l, int out, int in) {
+    l.out = out; l.in = in;
+    l.w = (const void*)(uintptr_t)off; off += (size_t)out * in;
+    l.b = (const void*)(uintptr_t)off; off += out;
+  };
+  Model& m = c->M;
+  take(m.img_in, H, C);
+  take(m.txt_in, H, X);
+  take(m.time0, H, g.time_dim);
+  take(m.time2, H, H);
+  if (g.pooled_text) { take(m.pool0, H, X); take(m.pool2, H, H); }
+  take(m.mod, c->n_mod, H);
+  m.dbl.resize(g.n_double);
+  for (auto& d : m.dbl)
+    for (int s = 0; s < 2; ++s) {
+      take(d.qkv[s], 3 * H, H); take(d.o[s], H, H); take(d.mlp0[s], F, H); take(d.mlp1[s], H, F);
+    }
+  m.sgl.resize(g.n_single);
+  for (auto& s : m.sgl) { take(s.l1, 3 * H + F, H); take(s.l2, H, H + F); }
+  m.crs.resize(g.n_cross);
+  for (auto& x : m.crs) {
+    x.mod_off = (const void*)(uintptr_t)off; off += 6 * (size_t)H;
+    take(x.qkv, 3 * H, H); take(x.o, H, H); take(x.xq, H, H); take(x.xkv, 2 * H, H); take(x.xo, H, H);
+    take(x.ffn0, F, H); take(x.ffn1, H, F);
+  }
+  take(m.fin, C, H);
+  *total_elems = off;
+  return DIT_OK;
+}
+
+void rebase(dit_cache* c) {
+  auto fix = [&](const void*& p) { p = (const char*)c->wdev + (uintptr_t)p * c->esz; };
+  auto fl = [&](Lin& l) { if (l.out) { fix(l.w); fix(l.b); } };
+  Model& m = c->M;
+  fl(m.img_in); fl(m.txt_in); fl(m.time0); fl(m.time2); fl(m.pool0); fl(m.pool2); fl(m.mod); fl(m.fin);
+  for (auto& d : m.dbl)
+    for (int s = 0; s < 2; ++s) { fl(d.qkv[s]); fl(d.o[s]); fl(d.mlp0[s]); fl(d.mlp1[s]); }
+  for (auto& s : m.sgl) { fl(s.l1); fl(s.l2); }
+  for (auto& x : m.crs) {
+    fix(x.mod_off);
+    fl(x.qkv); fl(x.o); fl(x.xq); fl(x.xkv); fl(x.xo); fl(x.ffn0); fl(x.ffn1);
+  }
+}
+
+dit_status validate(const dit_model_config* g, std::string& why) {
+  auto bad = [&](const char* m) { why = m; return DIT_ESHAPE; };
+  if (g->abi_version != DIT_ABI_VERSION) { why = "abi_version mismatch"; return DIT_EINVAL; }
+  if (g->dtype != DIT_DTYPE_F32 && g->dtype != DIT_DTYPE_BF16) { why = "bad dtype"; return DIT_EINVAL; }
+  if (g->n_double < 0 || g->n_single < 0 || g->n_cross < 0) return bad("negative block count");
+  if (g->n_double + g->n_single + g->n_cross < 1) return bad("no blocks");
+  if (g->n_cross && (g->n_double || g->n_single)) return bad("video blocks cannot mix with MMDiT blocks");
+  if (g->heads < 1 || g->head_dim < 1 || g->heads * g->head_dim != g->hidden) return bad("hidden != heads*head_dim");
+  if (g->mlp_hidden < 1 || g->in_channels < 1 || g->ctx_dim < 1 || g->time_dim < 2 || (g->time_dim & 1))
+    return bad("bad widths");
+  if (g->n_img < 1 || g->n_txt < 1) return bad("token counts must be >= 1");
+  if (g->batch != 1 && g->batch != 2) return bad("batch must be 1 or 2");
+  if (g->hidden > 8192) return bad("hidden > 8192");
+  if (g->dtype == DIT_DTYPE_BF16) {
+    if (g->head_dim != 128) return bad("bf16 path needs head_dim == 128");
+    if (g->hidden % 8 || g->mlp_hidden % 8 || g->ctx_dim % 8 || g->in_channels % 8 || g->time_dim % 8)
+      return bad("bf16 widths must be multiples of 8");
+  } else {
+    if (g->head_dim > 128 || (g->head_dim != 16 && g->head_dim != 32 && g->head_dim != 64 && g->head_dim != 128))
+      return bad("f32 path needs head_dim in {16, 32, 64, 128}");
+  }
+  return DIT_OK;
+}
+
+template <typename P>
+dit_status dalloc(dit_cache* c, P** p, size_t bytes) {
+  void* q = nullptr;
+  if (bytes == 0) bytes = 16;
+  hipError_t e = hipMalloc(&q, bytes);
+  if (e != hipSuccess) return fail(c, DIT_ENOMEM, "hipMalloc(" + std::to_string(bytes) + ") failed");
+  *p = (P*)q;
+  return DIT_OK;
+}
+
+dit_status alloc_workspace(dit_cache* c) {
+  const size_t e = c->esz;
+  const int H = c->H, N = c->N, L = c->L, Nt = c->Nt;
+  TRY(dalloc(c, &c->xs, (size_t)N * c->C * e));
+  TRY(dalloc(c, &c->h, (size_t)N * H * e));
+  for (auto& m : c->mbuf) TRY(dalloc(c, &m, (size_t)N * H * e));
+  TRY(dalloc(c, &c->r, (size_t)c->nb * N * H * e));
+  TRY(dalloc(c, &c->X, (size_t)L * H * e));
+  TRY(dalloc(c, &c->A, (size_t)L * H * e));
+  TRY(dalloc(c, &c->Y, (size_t)L * c->ldY * e));
+  if (c->bf16) TRY(dalloc(c, &c->vt, (size_t)c->cfg.heads * 128 * rup(L, 64) * 2));
+  TRY(dalloc(c, &c->hout, (size_t)N * H * e));
+  TRY(dalloc(c, &c->yf, (size_t)N * H * e));
+  TRY(dalloc(c, &c->vel, (size_t)c->nb * N * c->C * 4));
+  TRY(dalloc(c, &c->txt, (size_t)c->nb * Nt * H * e));
+  if (c->cfg.n_cross) {
+    TRY(dalloc(c, &c->ctxkv, (size_t)Nt * 2 * H * e));
+    if (c->bf16) TRY(dalloc(c, &c->vt2, (size_t)c->cfg.heads * 128 * rup(Nt, 64) * 2));
+  }
+  TRY(dalloc(c, &c->ones, (size_t)H * 4));
+  {
+    std::vector<float> one(H, 1.f);
+    HIPCK(hipMemcpy(c->ones, one.data(), H * 4, hipMemcpyHostToDevice));
+  }
+  c->max_partials = (N + 3) / 4 + 1;
+  TRY(dalloc(c, &c->partials, (size_t)c->max_partials * 4 * sizeof(double)));
+  HIPCK(hipHostMalloc((void**)&c->sums_host, 4 * sizeof(double), hipHostMallocMapped));
+  HIPCK(hipHostGetDevicePointer((void**)&c->sums_dev, c->sums_host, 0));
+  HIPCK(hipEventCreateWithFlags(&c->ev_sums, hipEventDisableTiming));
+  return DIT_OK;
+}
+
+void free_per_sample(dit_cache* c) {
+  void* ps[] = {c->mod, c->modx, c->temb, c->th, c->tv, c->pooled, c->ph, c->pv, c->svec, c->sig_dev};
+  for (void* p : ps)
+    if (p) hipFree(p);
+  c->mod = c->modx = c->tv = c->pv = nullptr;
+  c->temb = c->th = c->pooled = c->ph = c->svec = nullptr;
+  c->sig_dev = nullptr;
+  c->cap_T = 0;
+}
+
+dit_status ensure_T(dit_cache* c, int T) {
+  if (T <= c->cap_T) return DIT_OK;
+  free_per_sample(c);
+  const size_t e = c->esz;
+  const int H = c->H;
+  TRY(dalloc(c, &c->mod, (size_t)c->nb * T * c->n_mod * 4));
+  if (c->cfg.n_cross) TRY(dalloc(c, &c->modx, (size_t)c->nb * c->cfg.n_cross * T * 6 * H * 4));
+  TRY(dalloc(c, &c->temb, (size_t)T * c->cfg.time_dim * e));
+  TRY(dalloc(c, &c->th, (size_t)T * H * e));
+  TRY(dalloc(c, &c->tv, (size_t)T * H * 4));
+  TRY(dalloc(c, &c->pooled, (size_t)c->cfg.ctx_dim * e));
+  TRY(dalloc(c, &c->ph, (size_t)H * e));
+  TRY(dalloc(c, &c->pv, (size_t)H * 4));
+  TRY(dalloc(c, &c->svec, (size_t)T * H * e));
+  TRY(dalloc(c, &c->sig_dev, (size_t)(T + 1) * sizeof(double)));
+  c->cap_T = T;
+  return DIT_OK;
+}
+
+// ---------------------------------------------------------------- gate
+dit_status parse_gate(dit_cache* c, const float* blob, size_t n, GateMLP& g) {
+  if (!blob || n < 4) return fail(c, DIT_EINVAL, "gate blob missing or too short");
+  const double k = blob[0];
+  if (k < 2 || k > 16 || k != std::floor(k)) return fail(c, DIT_EINVAL, "gate blob: bad layer count");
+  const int kk = (int)k;
+  if (n < (size_t)(2 + kk)) return fail(c, DIT_EINVAL, "gate blob too short");
+  g.widths.resize(kk);
+  for (int i = 0; i < kk; ++i) {
+    const double w = blob[1 + i];
+    if (w < 1 || w > 4096 || w != std::floor(w)) return fail(c, DIT_EINVAL, "gate blob: bad width");
+    g.widths[i] = (int)w;
+  }
+  if (g.widths.back() != 1) return fail(c, DIT_EINVAL, "gate blob: output width must be 1");
+  if (g.widths[0] > DIT_N_FEATURES) return fail(c, DIT_EINVAL, "gate blob: more than 8 inputs");
+  size_t p = 1 + kk;
+  g.z = blob[p++] != 0.f;
+  size_t need = p + (g.z ? 2 * g.widths[0] : 0);
+  for (int i = 1; i < kk; ++i) need += (size_t)g.widths[i] * g.widths[i - 1] + g.widths[i];
+  if (need != n) return fail(c, DIT_EINVAL, "gate blob: length mismatch");
+  if (g.z) {
+    g.mu.assign(blob + p, blob + p + g.widths[0]); p += g.widths[0];
+    g.sd.assign(blob + p, blob + p + g.widths[0]); p += g.widths[0];
+  }
+  g.W.clear(); g.b.clear();
+  for (int i = 1; i < kk; ++i) {
+    const size_t nw = (size_t)g.widths[i] * g.widths[i - 1];
+    g.W.emplace_back(blob + p, blob + p + nw); p += nw;
+    g.b.emplace_back(blob + p, blob + p + g.widths[i]); p += g.widths[i];
+  }
+  return DIT_OK;
+}
+
+double gate_logit(const GateMLP& g, const double* f) {
+  std::vector<double> u(f, f + g.widths[0]), nx;
+  if (g.z)
+    for (int i = 0; i < g.widths[0]; ++i) u[i] = (u[i] - g.mu[i]) / g.sd[i];
+  const int nl = (int)g.W.size();
+  for (int l = 0; l < nl; ++l) {
+    const int o = g.widths[l + 1], in = g.widths[l];
+    nx.assign(o, 0.0);
+    for (int j = 0; j < o; ++j) {
+      double s = g.b[l][j];
+      for (int i = 0; i < in; ++i) s += g.W[l][(size_t)j * in + i] * u[i];
+      nx[j] = (l < nl - 1) ? (s > 0.0 ? s : 0.0) : s;
+    }
+    u.swap(nx);
+  }
+  return u[0];
+}
+
+// ---------------------------------------------------------------- steps
+struct StepCtx {
+  int t, T;
+  const float* modp[2];   // this step's modulation vector per branch
+  const float* modxp[2];  // video blocks: base of [n_cross][T][6H] per branch
+};
+
+dit_status full_stack(dit_cache* c, int b, const StepCtx& s) {
+  const int H = c->H, F = c->F, N = c->N, Nt = c->Nt, L = c->L, ldY = c->ldY;
+  const float* md = s.modp[b];
+  const void* txtb = sp(c, c->txt, (size_t)b * Nt * H);
+  char* Xi = sp(c, c->X, (size_t)Nt * H);  // image rows of the joint state
+  char* Ai = sp(c, c->A, (size_t)Nt * H);
+  char* Yi = sp(c, c->Y, (size_t)Nt * ldY);
+  const int cls = DIT_K_GEMM;
+
+  if (c->cfg.n_cross) {
+    HIPCK(hipMemcpyAsync(c->X, c->h, (size_t)N * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
+    for (int i = 0; i < c->cfg.n_cross; ++i) {
+      const CrossW& w = c->M.crs[i];
+      const float* e = s.modxp[b] + ((size_t)i * s.T + s.t) * 6 * H;
+      TRY(ln_mod(c, c->X, H, c->A, H, N, N, e, e + H, e, e + H, DIT_K_FULL_OTHER));
+      GemmArgs g = lin_args(c, c->A, H, w.qkv, c->Y, ldY, N);
+      g.rms_cols = 2 * H;
+      TRY(gemm(c, &g, 1, cls));
+      TRY(attention(c, c->Y, ldY, sp(c, c->Y, H), ldY, sp(c, c->Y, 2 * H), ldY, sp(c, c->Y, 3 * H), ldY, N,
+                    N, c->vt));
+      g = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.o, c->X, H, N, DIT_EPI_GATED_RES);
+      g.gate = e + 2 * H;
+      TRY(gemm(c, &g, 1, cls));
+      // cross-attention: q from LN(x), k/v from the text tokens
+      TRY(ln_mod(c, c->X, H, c->A, H, N, N, nullptr, nullptr, nullptr, nullptr, DIT_K_FULL_OTHER));
+      GemmArgs gq = lin_args(c, c->A, H, w.xq, c->Y, ldY, N);
+      gq.rms_cols = H;
+      GemmArgs gkv = lin_args(c, txtb, H, w.xkv, c->ctxkv, 2 * H, Nt);
+      gkv.rms_cols = H;
+      TRY(gemm(c, &gq, 1, cls));
+      TRY(gemm(c, &gkv, 1, cls));
+      TRY(attention(c, c->Y, ldY, c->ctxkv, 2 * H, sp(c, c->ctxkv, H), 2 * H, sp(c, c->Y, 3 * H), ldY, N, Nt,
+                    c->bf16 ? c->vt2 : nullptr));
+      g = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.xo, c->X, H, N, DIT_EPI_GATED_RES);
+      g.gate = c->ones;
+      TRY(gemm(c, &g, 1, cls));
+      TRY(ln_mod(c, c->X, H, c->A, H, N, N, e + 3 * H, e + 4 * H, e + 3 * H, e + 4 * H, DIT_K_FULL_OTHER));
+      g = lin_args(c, c->A, H, w.ffn0, sp(c, c->Y, 4 * H), ldY, N);
+      g.gelu_from = 0;
+      TRY(gemm(c, &g, 1, cls));
+      g = lin_args(c, sp(c, c->Y, 4 * H), ldY, w.ffn1, c->X, H, N, DIT_EPI_GATED_RES);
+      g.gate = e + 5 * H;
+      TRY(gemm(c, &g, 1, cls));
+    }
+    {
+      Scope sc(c, DIT_K_FULL_OTHER, 3.0 * N * H * c->esz);
+      TRY(typed(c, [&](auto* tp) {
+        using T = std::remove_pointer_t<decltype(tp)>;
+        return dit::launch_add<T>((const T*)c->X, (const T*)c->h, (T*)sp(c, c->r, (size_t)b * N * H),
+                                  (int64_t)N * H, -1.f, c->stream);
+      }));
+    }
+    return DIT_OK;
+  }
+
+  // MMDiT: X = [txt; img]
+  HIPCK(hipMemcpyAsync(c->X, txtb, (size_t)Nt * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
+  HIPCK(hipMemcpyAsync(Xi, c->h, (size_t)N * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
+  for (int i = 0; i < c->cfg.n_double; ++i) {
+    const DoubleW& w = c->M.dbl[i];
+    const float* mi = md + (size_t)12 * H * i;  // image stream chunk
+    const float* mt = mi + 6 * H;               // text stream chunk
+    TRY(ln_mod(c, c->X, H, c->A, H, L, Nt, mt, mt + H, mi, mi + H, DIT_K_FULL_OTHER));
+    GemmArgs g[2];
+    g[0] = lin_args(c, Ai, H, w.qkv[0], Yi, ldY, N);
+    g[1] = lin_args(c, c->A, H, w.qkv[1], c->Y, ldY, Nt);
+    g[0].rms_cols = g[1].rms_cols = 2 * H;
+    TRY(gemm(c, g, 2, cls));
+    TRY(attention(c, c->Y, ldY, sp(c, c->Y, H), ldY, sp(c, c->Y, 2 * H), ldY, sp(c, c->Y, 3 * H), ldY, L, L,
+                  c->vt));
+    g[0] = lin_args(c, Yi + 3 * H * c->esz, ldY, w.o[0], Xi, H, N, DIT_EPI_GATED_RES);
+    g[1] = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.o[1], c->X, H, Nt, DIT_EPI_GATED_RES);
+    g[0].gate = mi + 2 * H;
+    g[1].gate = mt + 2 * H;
+    TRY(gemm(c, g, 2, cls));
+    TRY(ln_mod(c, c->X, H, c->A, H, L, Nt, mt + 3 * H, mt + 4 * H, mi + 3 * H, mi + 4 * H, DIT_K_FULL_OTHER));
+    g[0] = lin_args(c, Ai, H, w.mlp0[0], Yi + 4 * H * c->esz, ldY, N);
+    g[1] = lin_args(c, c->A, H, w.mlp0[1], sp(c, c->Y, 4 * H), ldY, Nt);
+    g[0].gelu_from = g[1].gelu_from = 0;
+    TRY(gemm(c, g, 2, cls));
+    g[0] = lin_args(c, Yi + 4 * H * c->esz, ldY, w.mlp1[0], Xi, H, N, DIT_EPI_GATED_RES);
+    g[1] = lin_args(c, sp(c, c->Y, 4 * H), ldY, w.mlp1[1], c->X, H, Nt, DIT_EPI_GATED_RES);
+    g[0].gate = mi + 5 * H;
+    g[1].gate = mt + 5 * H;
+    TRY(gemm(c, g, 2, cls));
+  }
+  for (int i = 0; i < c->cfg.n_single; ++i) {
+    const SingleW& w = c->M.sgl[i];
+    const float* ms = md + (size_t)12 * H * c->cfg.n_double + (size_t)3 * H * i;
+    TRY(ln_mod(c, c->X, H, c->A, H, L, L, ms, ms + H, ms, ms + H, DIT_K_FULL_OTHER));
+    GemmArgs g = lin_args(c, c->A, H, w.l1, c->Y, ldY, L);
+    g.rms_cols = 2 * H;
+    g.gelu_from = 3 * H;
+    g.gap_at = 3 * H;
+    g.gap = H;
+    TRY(gemm(c, &g, 1, cls));
+    TRY(attention(c, c->Y, ldY, sp(c, c->Y, H), ldY, sp(c, c->Y, 2 * H), ldY, sp(c, c->Y, 3 * H), ldY, L, L,
+                  c->vt));
+    g = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.l2, c->X, H, L, DIT_EPI_GATED_RES);
+    g.gate = ms + 2 * H;
+    TRY(gemm(c, &g, 1, cls));
+  }
+  {
+    Scope sc(c, DIT_K_FULL_OTHER, 3.0 * N * H * c->esz);
+    TRY(typed(c, [&](auto* tp) {
+      using T = std::remove_pointer_t<decltype(tp)>;
+      return dit::launch_add<T>((const T*)Xi, (const T*)c->h, (T*)sp(c, c->r, (size_t)b * N * H),
+                                (int64_t)N * H, -1.f, c->stream);
+    }));
+  }
+  (void)F;
+  return DIT_OK;
+}
+
+// v_b = Final(h_out)
+dit_status final_layer(dit_cache* c, int b, const void* hout, const StepCtx& s, int cls) {
+  const int H = c->H, N = c->N;
+  const float* mf = s.modp[b] + (c->n_mod - 2 * H);
+  TRY(ln_mod(c, hout, H, c->yf, H, N, N, mf, mf + H, mf, mf + H, cls));
+  GemmArgs g = lin_args(c, c->yf, H, c->M.fin, c->vel + (size_t)b * N * c->C, c->C, N, DIT_EPI_F32);
+  Scope sc(c, cls, 0);
+  if (c->bf16) {
+    HIPCK(dit::launch_gemm_bf16(&g, 1, c->stream, c->n_cu));
+  } else {
+    HIPCK(dit::launch_gemm_f32(&g, 1, c->stream));
+  }
+  return DIT_OK;
+}
+
+// once per sample: text tokens, vec and the modulation table of every step
+dit_status prepare(dit_cache* c, const void* text_emb, const std::vector<double>& sig, int T) {
+  const int H = c->H, Nt = c->Nt, X = c->cfg.ctx_dim;
+  const int cls = DIT_K_ONCE;
+  HIPCK(hipMemcpyAsync(c->sig_dev, sig.data(), (T + 1) * sizeof(double), hipMemcpyHostToDevice, c->stream));
+  {
+    Scope s(c, cls, 0);
+    TRY(typed(c, [&](auto* tp) {
+      using Ty = std::remove_pointer_t<decltype(tp)>;
+      return dit::launch_time_embed<Ty>(c->sig_dev, (Ty*)c->temb, T, c->cfg.time_dim, c->stream);
+    }));
+  }
+  GemmArgs g = lin_args(c, c->temb, c->cfg.time_dim, c->M.time0, c->th, H, T, DIT_EPI_SILU);
+  TRY(gemm(c, &g, 1, cls));
+  g = lin_args(c, c->th, H, c->M.time2, c->tv, H, T, DIT_EPI_F32);
+  TRY(gemm(c, &g, 1, cls));
+  for (int b = 0; b < c->nb; ++b) {
+    const void* te = (const char*)text_emb + (size_t)b * Nt * X * c->esz;
+    g = lin_args(c, te, X, c->M.txt_in, sp(c, c->txt, (size_t)b * Nt * H), H, Nt);
+    TRY(gemm(c, &g, 1, cls));
+    if (b > 0 && !c->cfg.pooled_text) continue;  // identical vec and mod table
+    const float* pvp = nullptr;
+    if (c->cfg.pooled_text) {
+      {
+        Scope s(c, cls, 0);
+        TRY(typed(c, [&](auto* tp) {
+          using Ty = std::remove_pointer_t<decltype(tp)>;
+          return dit::launch_mean_rows<Ty>((const Ty*)te, Nt, X, (Ty*)c->pooled, c->stream);
+        }));
+      }
+      g = lin_args(c, c->pooled, X, c->M.pool0, c->ph, H, 1, DIT_EPI_SILU);
+      TRY(gemm(c, &g, 1, cls));
+      g = lin_args(c, c->ph, H, c->M.pool2, c->pv, H, 1, DIT_EPI_F32);
+      TRY(gemm(c, &g, 1, cls));
+      pvp = c->pv;
+    }
+    {
+      Scope s(c, cls, 0);
+      TRY(typed(c, [&](auto* tp) {
+        using Ty = std::remove_pointer_t<decltype(tp)>;
+        return dit::launch_vec_silu<Ty>(c->tv, pvp, (Ty*)c->svec, T, H, c->stream);
+      }));
+    }
+    g = lin_args(c, c->svec, H, c->M.mod, c->mod + (size_t)b * T * c->n_mod, c->n_mod, T, DIT_EPI_F32);
+    TRY(gemm(c, &g, 1, cls));
+    if (c->cfg.n_cross) {
+      const int base = 12 * H * c->cfg.n_double + 3 * H * c->cfg.n_single;
+      for (int i = 0; i < c->cfg.n_cross; ++i) {
+        Scope s(c, cls, 0);
+        float* dst = c->modx + ((size_t)b * c->cfg.n_cross + i) * T * 6 * H;
+        TRY(typed(c, [&](auto* tp) {
+          using Ty = std::remove_pointer_t<decltype(tp)>;
+          return dit::launch_add_offset<Ty>(c->mod + (size_t)b * T * c->n_mod, c->n_mod, base,
+                                            (const Ty*)c->M.crs[i].mod_off, dst, T, 6 * H, c->stream);
+        }));
+      }
+    }
+  }
+  return DIT_OK;
+}
+
+dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const GateMLP& gate,
+                      const dit_sample_params& p, dit_schedule* out) {
+  const int T = p.T, B = p.B;
+  const int H = c->H, N = c->N;
+  std::vector<double> sig(T + 1);
+  if (p.sigmas) {
+    for (int i = 0; i <= T; ++i) sig[i] = p.sigmas[i];
+  } else {
+    for (int i = 0; i <= T; ++i) {
+      const double u = 1.0 - (double)i / T;
+      sig[i] = p.shift * u / (1.0 + (p.shift - 1.0) * u);
+    }
+  }
+  TRY(ensure_T(c, T));
+  TRY(prepare(c, text_emb, sig, T));
+
+  StepCtx s{};
+  s.T = T;
+  const bool pair = c->nb == 2;
+  const double thr = std::log(p.tau / (1.0 - p.tau));
+  int cnt = 0, t_last = 0;
+  double acc = 0.0;
+  int i_prev = -1, i_last = -1;
+  out->nfe = 0;
+  out->steps_done = 0;
+
+  for (int t = 0; t < T; ++t) {
+    s.t = t;
+    for (int b = 0; b < c->nb; ++b) {
+      const int mb = (b > 0 && !c->cfg.pooled_text) ? 0 : b;
+      s.modp[b] = c->mod + ((size_t)mb * T + t) * c->n_mod;
+      s.modxp[b] = c->modx ? c->modx + (size_t)mb * c->cfg.n_cross * T * 6 * H : nullptr;
+    }
+    // (a1) patch embed and modulated indicator tensor, (a2) its sums
+    int i_new = 0;
+    while (i_new == i_prev || i_new == i_last) ++i_new;
+    const float *sh0 = nullptr, *sc0 = nullptr;
+    if (p.indicator == DIT_INDICATOR_MODULATED) {
+      if (c->cfg.n_cross) {
+        sh0 = s.modxp[0] + (size_t)t * 6 * H;  // block 0
+        sc0 = sh0 + H;
+      } else {
+        sh0 = s.modp[0];  // first block's image-stream (or single) shift
+        sc0 = sh0 + H;
+      }
+    }
+    int npart = 0;
+    {
+      Scope sc(c, DIT_K_INDICATOR, (double)N * H * c->esz * (t == 0 ? 2 : (i_prev == i_last ? 3 : 4)));
+      TRY(typed(c, [&](auto* tp) {
+        using Ty = std::remove_pointer_t<decltype(tp)>;
+        return dit::launch_cast_from_f32<Ty>(latent, (Ty*)c->xs, (int64_t)N * c->C, c->stream);
+      }));
+      GemmArgs g = lin_args(c, c->xs, c->C, c->M.img_in, c->h, H, N);
+      if (c->bf16) { HIPCK(dit::launch_gemm_bf16(&g, 1, c->stream, c->n_cu)); }
+      else { HIPCK(dit::launch_gemm_f32(&g, 1, c->stream)); }
+      TRY(typed(c, [&](auto* tp) {
+        using Ty = std::remove_pointer_t<decltype(tp)>;
+        return dit::launch_indicator<Ty>((const Ty*)c->h, (Ty*)c->mbuf[i_new],
+                                         t ? (const Ty*)c->mbuf[i_prev] : nullptr,
+                                         t ? (const Ty*)c->mbuf[i_last] : nullptr, N, H, sh0, sc0,
+                                         t ? c->partials : nullptr, &npart, c->stream);
+      }));
+      if (t) HIPCK(dit::launch_reduce_partials(c->partials, npart, c->sums_dev, c->stream));
+    }
+
+    // (a3) gate + pacing on the host
+    int dec = 1, forced = 1;
+    double z = NAN;
+    double f[DIT_N_FEATURES];
+    for (double& v : f) v = NAN;
+    double sums[4] = {NAN, NAN, NAN, NAN};
+    if (t > 0) {
+      HIPCK(hipEventRecord(c->ev_sums, c->stream));
+      HIPCK(hipEventSynchronize(c->ev_sums));
+      const auto h0 = std::chrono::steady_clock::now();
+      for (int k = 0; k < 4; ++k) sums[k] = ((volatile double*)c->sums_host)[k];
+      for (double v : sums)
+        if (!std::isfinite(v)) {
+          out->steps_done = t;
+          return fail(c, DIT_ENONFINITE, "indicator sum is not finite at step " + std::to_string(t));
+        }
+      const double d_prev = sums[0] / std::max(sums[1], 1e-30);
+      const double d_last = sums[2] / std::max(sums[3], 1e-30);
+      acc += d_prev;
+      f[0] = (double)B / T;
+      f[1] = (double)(B - cnt) / B;
+      f[2] = (double)(B - cnt) / (T - t);
+      f[3] = (double)(t - t_last);
+      f[4] = d_last;
+      f[5] = d_prev;
+      f[6] = (double)t / T;
+      f[7] = acc;
+      z = gate_logit(gate, f);
+      dec = (z > thr) ? 1 : 0;
+      forced = 0;
+      if (B - cnt >= T - t) { dec = 1; forced = 1; }
+      if (B - cnt == 0) { dec = 0; forced = 1; }
+      if (p.forced_mask) dec = p.forced_mask[t] ? 1 : 0;
+      c->stats.host_gate_ms +=
+          std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - h0).count();
+    }
+    out->full[t] = (uint8_t)dec;
+    if (out->logit) out->logit[t] = (float)z;
+    if (out->forced) out->forced[t] = (uint8_t)forced;
+    if (out->features)
+      for (int k = 0; k < DIT_N_FEATURES; ++k) out->features[(size_t)t * DIT_N_FEATURES + k] = f[k];
+    if (out->sums)
+      for (int k = 0; k < 4; ++k) out->sums[(size_t)t * 4 + k] = sums[k];
+
+    // (a4) full or reuse, (a5) final layer + Euler
+    for (int b = 0; b < c->nb; ++b) {
+      if (dec) {
+        TRY(full_stack(c, b, s));
+        const void* hout = c->cfg.n_cross ? c->X : sp(c, c->X, (size_t)c->Nt * H);
+        TRY(final_layer(c, b, hout, s, DIT_K_FULL_OTHER));
+      } else {
+        {
+          Scope sc(c, DIT_K_REUSE, 3.0 * N * H * c->esz);
+          TRY(typed(c, [&](auto* tp) {
+            using Ty = std::remove_pointer_t<decltype(tp)>;
+            return dit::launch_add<Ty>((const Ty*)c->h, (const Ty*)sp(c, c->r, (size_t)b * N * H),
+                                       (Ty*)c->hout, (int64_t)N * H, 1.f, c->stream);
+          }));
+        }
+        TRY(final_layer(c, b, c->hout, s, DIT_K_REUSE));
+      }
+    }
+    {
+      Scope sc(c, dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
+      const float dsig = (float)(sig[t + 1] - sig[t]);
+      HIPCK(dit::launch_euler(latent, c->vel, pair ? c->vel + (size_t)N * c->C : nullptr,
+                              (float)p.guidance, dsig, (int64_t)N * c->C, c->stream));
+    }
+    if (dec) {
+      cnt += 1;
+      t_last = t;
+      acc = 0.0;
+      i_last = i_new;
+      c->stats.full_steps += 1;
+    } else {
+      c->stats.reuse_steps += 1;
+    }
+    i_prev = i_new;
+    out->nfe = cnt;
+    out->steps_done = t + 1;
+  }
+  HIPCK(hipStreamSynchronize(c->stream));
+  if (cnt != B) return fail(c, DIT_EBUDGET, "realised NFE differs from the budget");
+  return DIT_OK;
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+extern "C" {
+
+dit_status dit_cache_create(const dit_model_config* cfg, const void* weights, size_t nbytes, void* hip_stream,
+                            dit_cache** out) {
+  g_create_error.clear();
+  if (!cfg || !weights || !out) return fail(nullptr, DIT_EINVAL, "null argument");
+  *out = nullptr;
+  std::string why;
+  dit_status st = validate(cfg, why);
+  if (st != DIT_OK) return fail(nullptr, st, why);
+  dit_cache* c = new dit_cache();
+  c->cfg = *cfg;
+  c->stream = (hipStream_t)hip_stream;
+  c->bf16 = cfg->dtype == DIT_DTYPE_BF16;
+  c->esz = c->bf16 ? 2 : 4;
+  c->H = cfg->hidden; c->F = cfg->mlp_hidden; c->N = cfg->n_img; c->Nt = cfg->n_txt;
+  c->L = cfg->n_cross ? cfg->n_img : cfg->n_img + cfg->n_txt;
+  c->C = cfg->in_channels; c->nb = cfg->batch;
+  c->n_mod = 12 * c->H * cfg->n_double + 3 * c->H * cfg->n_single + (cfg->n_cross ? 6 * c->H : 0) + 2 * c->H;
+  c->ldY = 4 * c->H + c->F;
+  int dev = 0;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) c->n_cu = n;
+  }
+  size_t elems = 0;
+  layout(c, &elems);
+  if (elems * c->esz != nbytes) {
+    std::string m = "weight blob is " + std::to_string(nbytes) + " bytes, layout needs " +
+                    std::to_string(elems * c->esz);
+    delete c;
+    return fail(nullptr, DIT_ESHAPE, m);
+  }
+  c->wbytes = nbytes;
+  st = dalloc(c, &c->wdev, nbytes);
+  if (st == DIT_OK) st = alloc_workspace(c);
+  if (st == DIT_OK) {
+    hipError_t e = hipMemcpyAsync(c->wdev, weights, nbytes, hipMemcpyHostToDevice, c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) st = fail(c, DIT_EHIP, std::string("weight upload: ") + hipGetErrorString(e));
+  }
+  if (st != DIT_OK) {
+    g_create_error = c->err;
+    dit_cache_destroy(c);
+    return st;
+  }
+  rebase(c);
+  *out = c;
+  return DIT_OK;
+}
+
+dit_status dit_cache_sample_ex(dit_cache* c, float* latent, const void* text_emb, const float* gate_weights,
+                               size_t gate_len, const dit_sample_params* p, dit_schedule* out) {
+  if (!c) return DIT_EINVAL;
+  c->err.clear();
+  if (!latent || !text_emb || !p || !out || !out->full) return fail(c, DIT_EINVAL, "null argument");
+  out->nfe = 0;
+  out->steps_done = 0;
+  if (p->T < 1 || p->B < 1 || p->B > p->T) return fail(c, DIT_EBUDGET, "need 1 <= B <= T");
+  if (!(p->tau > 0.0 && p->tau < 1.0)) return fail(c, DIT_EINVAL, "tau must be in (0, 1)");
+  if (p->indicator != DIT_INDICATOR_MODULATED && p->indicator != DIT_INDICATOR_PATCH)
+    return fail(c, DIT_EINVAL, "bad indicator");
+  if (!p->sigmas && !(p->shift > 0.0)) return fail(c, DIT_EINVAL, "shift must be > 0");
+  if (p->forced_mask) {
+    int ones = 0;
+    for (int t = 0; t < p->T; ++t) {
+      if (p->forced_mask[t] > 1) return fail(c, DIT_EINVAL, "forced mask entries must be 0/1");
+      ones += p->forced_mask[t];
+    }
+    if (p->forced_mask[0] != 1 || ones != p->B) return fail(c, DIT_EINVAL, "forced mask needs m_0 = 1 and B ones");
+  }
+  GateMLP gate;
+  TRY(parse_gate(c, gate_weights, gate_len, gate));
+  const auto t0 = std::chrono::steady_clock::now();
+  dit_status st = run_sample(c, latent, text_emb, gate, *p, out);
+  if (st != DIT_OK) hipStreamSynchronize(c->stream);
+  collect_events(c);
+  c->stats.sample_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  c->stats.samples += (st == DIT_OK);
+  return st;
+}
+
+dit_status dit_cache_sample(dit_cache* c, float* latent, const void* text_emb, int32_t T, int32_t B,
+                            const float* gate_weights, size_t gate_len, dit_schedule* out) {
+  dit_sample_params p{};
+  p.T = T; p.B = B; p.sigmas = nullptr; p.shift = 1.0; p.tau = 0.5; p.guidance = 1.0;
+  p.forced_mask = nullptr; p.indicator = DIT_INDICATOR_MODULATED;
+  return dit_cache_sample_ex(c, latent, text_emb, gate_weights, gate_len, &p, out);
+}
+
+void dit_cache_destroy(dit_cache* c) {
+  if (!c) return;
+  if (c->stream) hipStreamSynchronize(c->stream);
+  free_per_sample(c);
+  void* ps[] = {c->wdev, c->xs, c->h, c->mbuf[0], c->mbuf[1], c->mbuf[2], c->r, c->X, c->A, c->Y, c->vt,
+                c->hout, c->yf, c->vel, c->txt, c->ctxkv, c->vt2, c->ones, c->partials};
+  for (void* p : ps)
+    if (p) hipFree(p);
+  if (c->sums_host) hipHostFree(c->sums_host);
+  if (c->ev_sums) hipEventDestroy(c->ev_sums);
+  for (hipEvent_t e : c->ev_pool) hipEventDestroy(e);
+  delete c;
+}
+
+const char* dit_cache_last_error(const dit_cache* c) {
+  return c ? c->err.c_str() : g_create_error.c_str();
+}
+
+dit_status dit_cache_set_profiling(dit_cache* c, int32_t enable) {
+  if (!c) return DIT_EINVAL;
+  c->prof = enable != 0;
+  return DIT_OK;
+}
+
+dit_status dit_cache_get_stats(const dit_cache* c, dit_stats* out) {
+  if (!c || !out) return DIT_EINVAL;
+  *out = c->stats;
+  return DIT_OK;
+}
+
+dit_status dit_cache_reset_stats(dit_cache* c) {
+  if (!c) return DIT_EINVAL;
+  c->stats = dit_stats{};
+  return DIT_OK;
+}
+
+// ---------------------------------------------------------------- components
+dit_status dit_gemm_bf16(const dit_gemm_desc* d, void* hip_stream) {
+  dit_cache* c = nullptr;
+  if (!d || !d->A || !d->W || !d->C) return fail(c, DIT_EINVAL, "null argument");
+  if (d->flags & ~(DIT_EPI_F32 | DIT_EPI_GATED_RES | DIT_EPI_SILU)) return fail(c, DIT_EINVAL, "bad flags");
+  if ((d->flags & DIT_EPI_GATED_RES) && (!d->gate || (d->flags & DIT_EPI_F32)))
+    return fail(c, DIT_EINVAL, "gated residual needs a gate and bf16 output");
+  if (d->M < 0 || d->N < 0 || d->K < 1 || d->K % 8 || d->lda < d->K || d->ldw < d->K)
+    return fail(c, DIT_ESHAPE, "bad GEMM shape");
+  if (d->rms_cols < 0 || d->rms_cols % 128) return fail(c, DIT_ESHAPE, "rms_cols must be a multiple of 128");
+  GemmArgs g{};
+  g.A = d->A; g.lda = d->lda; g.W = d->W; g.ldw = d->ldw; g.bias = d->bias;
+  g.C = d->C; g.ldc = d->ldc; g.gate = d->gate; g.M = d->M; g.N = d->N; g.K = d->K;
+  g.flags = d->flags; g.rms_cols = d->rms_cols;
+  g.gelu_from = d->gelu_from; g.gap_at = d->gap ? d->gap_at : 0x7fffffff; g.gap = d->gap;
+  int dev = 0, ncu = 256;
+  hipGetDevice(&dev);
+  hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+  hipStream_t s = (hipStream_t)hip_stream;
+  HIPCK(dit::launch_gemm_bf16(&g, 1, s, ncu));
+  HIPCK(hipStreamSynchronize(s));
+  return DIT_OK;
+}
+
+dit_status dit_attention_bf16(const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v, int64_t ldv,
+                              void* o, int64_t ldo, int32_t Lq, int32_t Lk, int32_t heads, void* vt_ws,
+                              void* hip_stream) {
+  dit_cache* c = nullptr;
+  if (!q || !k || !v || !o || !vt_ws) return fail(c, DIT_EINVAL, "null argument");
+  if (Lq < 1 || Lk < 1 || heads < 1) return fail(c, DIT_ESHAPE, "bad attention shape");
+  if (ldq < heads * 128 || ldk < heads * 128 || ldv < heads * 128 || ldo < heads * 128)
+    return fail(c, DIT_ESHAPE, "row stride smaller than heads*128");
+  hipStream_t s = (hipStream_t)hip_stream;
+  HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt_ws, Lk, heads, s));
+  HIPCK(dit::launch_flash_attn_bf16(q, ldq, k, ldk, vt_ws, (int)rup(Lk, 64), o, ldo, Lq, Lk, heads, s));
+  HIPCK(hipStreamSynchronize(s));
+  return DIT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,84 @@
+// Internal launchers of the gfx950 kernels (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/dit_kernels.h"
+
+namespace dit {
+
+struct GemmArgs {
+  const void* A; int64_t lda;
+  const void* W; int64_t ldw;
+  const void* bias;
+  void* C; int64_t ldc;
+  const float* gate;
+  int M, N, K;
+  int flags;
+  int rms_cols = 0;
+  int gelu_from = 0x7fffffff;
+  int gap_at = 0x7fffffff;
+  int gap = 0;
+};
+
+// bf16 MFMA GEMM; n = 1 or 2 independent problems in one launch.
+hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t s, int n_cu);
+// f32 GEMM (small f32 workloads); bias f32; rms_cols handled by rms_heads_f32.
+hipError_t launch_gemm_f32(const GemmArgs* g, int n, hipStream_t s);
+
+// Flash attention, bf16, head_dim 128. vt = v transposed per head:
+// [heads][128][ldvt], ldvt = round_up(Lk, 64), zero padded.
+hipError_t launch_transpose_v_bf16(const void* v, int64_t ldv, void* vt, int Lk, int heads,
+                                   hipStream_t s);
+hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int64_t ldk,
+                                  const void* vt, int ldvt, void* o, int64_t ldo, int Lq,
+                                  int Lk, int heads, hipStream_t s);
+// f32 attention, head_dim <= 128 (multiple of 4).
+hipError_t launch_attn_f32(const float* q, int64_t ldq, const float* k, int64_t ldk,
+                           const float* v, int64_t ldv, float* o, int64_t ldo, int Lq, int Lk,
+                           int heads, int head_dim, hipStream_t s);
+
+// ---- streaming kernels, templated on the storage type (float or bf16) ----
+// out = S(LN(x) * (1 + scale) + shift) per row; rows < split use (sh0, sc0),
+// the others (sh1, sc1); mod vectors are f32.  scale == nullptr: plain LN.
+template <typename T>
+hipError_t launch_ln_mod(const T* x, int64_t ldx, T* out, int64_t ldo, int rows, int H, int split,
+                         const float* sh0, const float* sc0, const float* sh1, const float* sc1,
+                         hipStream_t s);
+// Indicator: m = S(LN(h)(1+sc)+sh) (or m = h when sc == nullptr), written
+// to m_out; per-block partial sums (f64) of |m-mp|, |mp|, |m-ml|, |ml|.
+template <typename T>
+hipError_t launch_indicator(const T* h, T* m_out, const T* m_prev, const T* m_last, int rows,
+                            int H, const float* sh, const float* sc, double* partials,
+                            int* n_partials, hipStream_t s);
+// Fixed-order f64 reduction of n partial 4-vectors into out[4] (host-mapped).
+hipError_t launch_reduce_partials(const double* partials, int n, double* out, hipStream_t s);
+// r = S(a - b) (refresh) or r = S(a + b) (reuse), n elements.
+template <typename T>
+hipError_t launch_add(const T* a, const T* b, T* out, int64_t n, float sign, hipStream_t s);
+// x += dsigma * v (batch 1) or x += dsigma * (v_u + g (v_c - v_u)).
+hipError_t launch_euler(float* x, const float* v_c, const float* v_u, float g, float dsigma,
+                        int64_t n, hipStream_t s);
+// latent f32 -> storage type.
+template <typename T>
+hipError_t launch_cast_from_f32(const float* x, T* out, int64_t n, hipStream_t s);
+// Per-head RMS norm in place on columns [0, cols) of rows x ld (f32 path).
+hipError_t launch_rms_heads_f32(float* x, int64_t ld, int rows, int cols, int head_dim,
+                                hipStream_t s);
+// temb[t][k] = S(cos / sin(1000 sigma_t f_k)), f_k = 10000^(-k/half).
+template <typename T>
+hipError_t launch_time_embed(const double* sigmas, T* out, int T_, int dim, hipStream_t s);
+// out[c] = S(mean over rows of x[:, c]).
+template <typename T>
+hipError_t launch_mean_rows(const T* x, int rows, int cols, T* out, hipStream_t s);
+// out[t][c] = S(SiLU(S(a[t][c] + (b ? b[c] : 0)))) with a f32 [rows, cols], b f32 [cols].
+template <typename T>
+hipError_t launch_vec_silu(const float* a, const float* b, T* out, int rows, int cols,
+                           hipStream_t s);
+// mod_blk[t][c] = mod[t][base + c] + offset[c] (video blocks), f32.
+template <typename T>
+hipError_t launch_add_offset(const float* mod, int64_t ld, int base, const T* offset, float* out,
+                             int rows, int cols, hipStream_t s);
+
+}  // namespace dit

@@ -1,0 +1,116 @@
+"""End-to-end GPU parity of the cached sampler against the oracle.
+
+Protocol (the two sides can legitimately disagree only on decisions whose
+gate logit is within 1e-3 of the threshold): run the device sampler with the
+gate, replay its schedule in the oracle, then require (a) identical
+decisions wherever the oracle's logit clears the margin, (b) NFE = B and
+m_0 = 1, (c) final latents within rel-L2 1e-5 (f32) / 2e-2 (bf16), (d)
+matching indicator sums and features.  Where no near-tie occurs, the
+oracle's own gated run must give the identical schedule."""
+import numpy as np
+import pytest
+
+from oracle import sample as oracle_sample
+from paper_2608_09231_amd import binding, synth
+from tests._gpu import check_schedule_against_oracle, rel_l2, run_sampler, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+SUM_TOL = {"f32": 1e-5, "bf16": 1e-3}
+
+
+def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5):
+    torch = torch_cuda()
+    w = synth.workload(name)
+    cfg = w.model
+    weights, x0, text, gate = synth.make_inputs(w)
+    T = T or w.T
+    B = B or w.B
+    x_gpu, sched, h = run_sampler(torch, w, weights, x0, text, gate, T=T, B=B, indicator=indicator, tau=tau)
+    h.close()
+    assert sched.nfe == B and int(sched.full.sum()) == B and sched.full[0] == 1
+    ores = oracle_sample(cfg, weights.tensors, gate, x0, text, T, B, shift=w.shift, tau=tau,
+                         guidance=w.guidance, forced_mask=sched.full, indicator=indicator)
+    check_schedule_against_oracle(sched, ores)
+    err = rel_l2(x_gpu, ores.x)
+    assert err <= TOL[cfg.dtype], err
+    ok = np.isfinite(ores.sums[1:])
+    np.testing.assert_allclose(sched.sums[1:][ok], ores.sums[1:][ok], rtol=SUM_TOL[cfg.dtype])
+    np.testing.assert_allclose(sched.features[1:, :4], ores.features[1:, :4], rtol=1e-12)
+    np.testing.assert_allclose(sched.features[1:, 4:], ores.features[1:, 4:], rtol=10 * SUM_TOL[cfg.dtype])
+    gated = oracle_sample(cfg, weights.tensors, gate, x0, text, T, B, shift=w.shift, tau=tau,
+                          guidance=w.guidance, indicator=indicator)
+    if np.all(np.abs(ores.logit[1:]) > 1e-3):
+        np.testing.assert_array_equal(sched.full, gated.full)
+    return sched, ores, err
+
+
+def test_tiny_f32_parity():
+    sched, ores, err = parity("tiny")
+    print("tiny rel-L2", err, "schedule", sched.full.tolist())
+
+
+def test_small_f32_parity():
+    parity("small_f32")
+
+
+def test_small_bf16_parity():
+    sched, ores, err = parity("small_bf16")
+    print("small_bf16 rel-L2", err, "schedule", sched.full.tolist())
+
+
+def test_small_bf16_patch_indicator():
+    parity("small_bf16", indicator="patch")
+
+
+def test_small_cfg_bf16_parity():
+    parity("small_cfg_bf16")
+
+
+def test_small_cross_bf16_parity():
+    parity("small_cross_bf16")
+
+
+def test_budget_edges_tiny():
+    for T, B in ((1, 1), (6, 6), (7, 1)):
+        parity("tiny", T=T, B=B)
+
+
+def test_forced_replay_and_determinism():
+    torch = torch_cuda()
+    w = synth.workload("small_bf16")
+    weights, x0, text, gate = synth.make_inputs(w)
+    x1, s1, h = run_sampler(torch, w, weights, x0, text, gate)
+    x2, s2, _ = run_sampler(torch, w, weights, x0, text, gate, handle=h)
+    x3, s3, _ = run_sampler(torch, w, weights, x0, text, gate, forced=s1.full, handle=h)
+    h.close()
+    np.testing.assert_array_equal(x1, x2)
+    np.testing.assert_array_equal(s1.full, s2.full)
+    np.testing.assert_array_equal(s1.sums[1:], s2.sums[1:])
+    np.testing.assert_array_equal(x1, x3)
+
+
+def test_error_paths_on_device():
+    torch = torch_cuda()
+    w = synth.workload("tiny")
+    weights, x0, text, gate = synth.make_inputs(w)
+    h = binding.DitCache(w.model, weights.blob)
+    lat = torch.from_numpy(x0).cuda()
+    txt = torch.from_numpy(text).cuda()
+    for T, B in ((5, 0), (5, 6), (0, 0)):
+        with pytest.raises(binding.DitError) as e:
+            h.sample(lat, txt, gate, T, B)
+        assert e.value.status == binding.DIT_EBUDGET
+    with pytest.raises(binding.DitError) as e:
+        h.sample(lat, txt, gate[:-1], 5, 2)
+    assert e.value.status == binding.DIT_EINVAL
+    with pytest.raises(binding.DitError) as e:
+        h.sample(lat, txt, gate, 5, 2, forced_mask=[0, 1, 1, 0, 0])
+    assert e.value.status == binding.DIT_EINVAL
+    bad = lat.clone()
+    bad[3, 2] = float("nan")
+    with pytest.raises(binding.DitError) as e:
+        h.sample(bad, txt, gate, 5, 2)
+    assert e.value.status == binding.DIT_ENONFINITE
+    h.close()
