@@ -21,157 +21,199 @@ namespace {
 
 constexpr int D = 128;
 constexpr int KT = 64;        // keys per tile
-constexpr int KLD = D + 8;    // padded K row, elements
-constexpr int VLD = KT + 8;   // padded V^T row, elements (144 bytes)
-constexpr int QW = 32;        // queries per wave
-constexpr int QB = 4 * QW;    // queries per workgroup
+constexpr int QG = 2;         // 32-query groups per wave
+constexpr int QW = 32 * QG;   // queries per wave
+constexpr int NW = 4;         // waves per workgroup
+constexpr int QB = NW * QW;   // queries per workgroup
+constexpr float RESCALE_SLACK = 8.f;  // log2 units a stale max may lag behind
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+// Position of key k (0..15) inside its 16-key group of the transposed V:
+// the two 4-key runs a lane half needs for one MFMA k-step become adjacent.
+__host__ __device__ constexpr int vt_slot(int k) { return 8 * ((k >> 2) & 1) + 4 * (k >> 3) + (k & 3); }
+
+// LDS tiles (bf16, no padding): K [64 keys][128 d], 16-byte chunk c of row r
+// stored at chunk c ^ (r & 15); V^T [128 d][64 keys], chunk c of row d at
+// c ^ ((d >> 1) & 7).  Both make the MFMA operand reads of 16 consecutive
+// rows hit 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int k_off(int row, int c) { return row * 256 + ((c ^ (row & 15)) << 4); }
+__device__ __forceinline__ int v_off(int d, int c) { return d * 128 + ((c ^ ((d >> 1) & 7)) << 4); }
 
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void flash_attn_bf16_kernel(
     const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restrict__ k, int64_t ldk,
     const bf16_t* __restrict__ vt, int ldvt, bf16_t* __restrict__ o, int64_t ldo, int Lq, int Lk,
     float scale_log2) {
-  __shared__ __attribute__((aligned(16))) bf16_t sK[2][KT * KLD];
-  __shared__ __attribute__((aligned(16))) bf16_t sV[2][D * VLD];
+  __shared__ __attribute__((aligned(1024))) char smem[2][2 * KT * D * 2];  // [stage][K | V^T]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lrow = lane & 31, lhalf = lane >> 5;
   const int h = blockIdx.y;
-  const int qi = blockIdx.x * QB + wave * QW + lrow;
-  const int qrow = min(qi, Lq - 1);
+  const int q0 = blockIdx.x * QB + wave * QW;
 
-  // Q^T fragments: lane holds d = 16 s + 8 lhalf + [0, 8) of its query.
-  bf16x8_t qf[8];
-  {
-    const bf16_t* qp = q + (int64_t)qrow * ldq + h * D + 8 * lhalf;
+  // Q^T fragments (B operand): lane holds d = 16 s + 8 lhalf + [0, 8) of query q0 + 32 g + lrow.
+  bf16x8_t qf[QG][8];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) qf[s] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(qp + 16 * s));
+  for (int g = 0; g < QG; ++g) {
+    const int qr = min(q0 + 32 * g + lrow, Lq - 1);
+    const bf16_t* qp = q + (int64_t)qr * ldq + h * D + 8 * lhalf;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qf[g][s] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(qp + 16 * s));
   }
 
   const bf16_t* kh = k + h * D;
   const bf16_t* vh = vt + (int64_t)h * D * ldvt;
-  uint4 rk[4], rv[4];
-  auto gload = [&](int kb0) {
+  // Direct global -> LDS copies: each instruction moves 64 x 16 bytes to a
+  // contiguous 1 KB; the lane -> (row, chunk) choice realises the swizzle.
+  auto issue_tile = [&](int kb0, int st) {
+    char* sk = smem[st];
+    char* sv = smem[st] + KT * D * 2;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i;
-      const int key = min(kb0 + (c >> 4), Lk - 1);
-      rk[i] = *(const uint4*)(kh + (int64_t)key * ldk + (c & 15) * 8);
-      const int d = c >> 3;
-      rv[i] = *(const uint4*)(vh + (int64_t)d * ldvt + kb0 + (c & 7) * 8);
-    }
-  };
-  auto sstore = [&](int st) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i;
-      *(uint4*)(&sK[st][(c >> 4) * KLD + (c & 15) * 8]) = rk[i];
-      *(uint4*)(&sV[st][(c >> 3) * VLD + (c & 7) * 8]) = rv[i];
+    for (int j = 0; j < 4; ++j) {
+      const int ii = wave * 4 + j;
+      {  // K rows 4 ii .. 4 ii + 3
+        const int row = 4 * ii + (lane >> 4);
+        const int c = (lane & 15) ^ (row & 15);
+        const int key = min(kb0 + row, Lk - 1);
+        __builtin_amdgcn_global_load_lds((glb_void_t*)(kh + (int64_t)key * ldk + c * 8),
+                                         (lds_void_t*)(sk + ii * 1024), 16, 0, 0);
+      }
+      {  // V^T rows 8 ii .. 8 ii + 7
+        const int d = 8 * ii + (lane >> 3);
+        const int c = (lane & 7) ^ ((d >> 1) & 7);
+        __builtin_amdgcn_global_load_lds((glb_void_t*)(vh + (int64_t)d * ldvt + kb0 + c * 8),
+                                         (lds_void_t*)(sv + ii * 1024), 16, 0, 0);
+      }
     }
   };
 
-  f32x16_t oacc[4];
+  f32x16_t oacc[QG][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int g = 0; g < QG; ++g)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[g][i][r] = 0.f;
+  float m_run[QG], l_run[QG];
+#pragma unroll
+  for (int g = 0; g < QG; ++g) { m_run[g] = -INFINITY; l_run[g] = 0.f; }
 
   const int ntiles = (Lk + KT - 1) / KT;
-  gload(0);
-  sstore(0);
+  issue_tile(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   for (int t = 0; t < ntiles; ++t) {
     const int st = t & 1;
-    if (t + 1 < ntiles) gload((t + 1) * KT);
+    if (t + 1 < ntiles) issue_tile((t + 1) * KT, st ^ 1);
+    const char* sk = smem[st];
+    const char* sv = smem[st] + KT * D * 2;
 
-    // S^T = K Q^T for 64 keys: two 32-key tiles.
-    f32x16_t sacc[2];
+    // S^T = K Q^T: 64 keys x 32 queries per group
+    f32x16_t sacc[QG][2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int g = 0; g < QG; ++g)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-      const bf16_t* kp = &sK[st][(kb * 32 + lrow) * KLD + 8 * lhalf];
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *(const uint4*)(kp + 16 * s));
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
-      }
-    }
-    // scale, mask, running max
-    const int kbase = t * KT;
-    float mx = -INFINITY;
+        for (int r = 0; r < 16; ++r) sacc[g][kb][r] = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kbase + kb * 32 + 8 * (r >> 2) + 4 * lhalf + (r & 3);
-        float v = sacc[kb][r] * scale_log2;
-        v = key < Lk ? v : -INFINITY;
-        sacc[kb][r] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    float ls = 0.f;
-    bf16x8_t pf[4];
+      for (int s = 0; s < 8; ++s) {
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sk + k_off(kb * 32 + lrow, 2 * s + lhalf)));
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      uint32_t w[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float p0 = __builtin_amdgcn_exp2f(sacc[kb][2 * j] - m_new);
-        const float p1 = __builtin_amdgcn_exp2f(sacc[kb][2 * j + 1] - m_new);
-        ls += p0 + p1;
-        w[j] = (uint32_t)f32_to_bf16(p0) | ((uint32_t)f32_to_bf16(p1) << 16);
+        for (int g = 0; g < QG; ++g)
+          sacc[g][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[g][s], sacc[g][kb], 0, 0, 0);
       }
-      pf[2 * kb] = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
-      pf[2 * kb + 1] = __builtin_bit_cast(bf16x8_t, make_uint4(w[4], w[5], w[6], w[7]));
+
+    const int kbase = t * KT;
+    const bool ragged = kbase + KT > Lk;
+    bf16x8_t pf[QG][4];
+#pragma unroll
+    for (int g = 0; g < QG; ++g) {
+      if (ragged) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kbase + kb * 32 + 8 * (r >> 2) + 4 * lhalf + (r & 3);
+            if (key >= Lk) sacc[g][kb][r] = -INFINITY;
+          }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[g][kb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * scale_log2;
+      // Keep a stale running max unless the new one is more than
+      // RESCALE_SLACK above it (exact: softmax is shift invariant).
+      const bool need = mx > m_run[g] + RESCALE_SLACK;
+      if (__builtin_amdgcn_ballot_w64(need)) {
+        const float m_new = need ? mx : m_run[g];
+        const float alpha = __builtin_amdgcn_exp2f(m_run[g] - m_new);
+        l_run[g] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[g][dt][r] *= alpha;
+        m_run[g] = m_new;
+      }
+      const float mneg = -m_run[g];
+      float ls = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        uint32_t w[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[g][kb][2 * j], scale_log2, mneg));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[g][kb][2 * j + 1], scale_log2, mneg));
+          ls += p0 + p1;
+          w[j] = pack_bf16x2(p0, p1);
+        }
+        pf[g][2 * kb] = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
+        pf[g][2 * kb + 1] = __builtin_bit_cast(bf16x8_t, make_uint4(w[4], w[5], w[6], w[7]));
+      }
+      l_run[g] += ls;
     }
-    l_run = l_run * alpha + ls;
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
 
     // O^T += V^T P^T
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
-      const bf16_t* vp = &sV[st][(dt * 32 + lrow) * VLD + 4 * lhalf];
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const uint2 lo = *(const uint2*)(vp + 16 * ks);
-        const uint2 hi = *(const uint2*)(vp + 16 * ks + 8);
-        const uint4 v4 = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, v4), pf[ks],
-                                                          oacc[dt], 0, 0, 0);
+        const bf16x8_t vf =
+            __builtin_bit_cast(bf16x8_t, *(const uint4*)(sv + v_off(dt * 32 + lrow, 2 * ks + lhalf)));
+#pragma unroll
+        for (int g = 0; g < QG; ++g)
+          oacc[g][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[g][ks], oacc[g][dt], 0, 0, 0);
       }
-    }
-    if (t + 1 < ntiles) sstore(st ^ 1);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   }
 
-  const float l = l_run + __shfl_xor(l_run, 32, 64);
-  const float inv = 1.f / l;
-  if (qi < Lq) {
-    bf16_t* op = o + (int64_t)qi * ldo + h * D;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+  for (int g = 0; g < QG; ++g) {
+    const int qi = q0 + 32 * g + lrow;
+    const float l = l_run[g] + __shfl_xor(l_run[g], 32, 64);
+    const float inv = 1.f / l;
+    if (qi < Lq) {
+      bf16_t* op = o + (int64_t)qi * ldo + h * D;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int d0 = dt * 32 + 8 * g + 4 * lhalf;
-        uint32_t w0 = (uint32_t)f32_to_bf16(oacc[dt][4 * g] * inv) |
-                      ((uint32_t)f32_to_bf16(oacc[dt][4 * g + 1] * inv) << 16);
-        uint32_t w1 = (uint32_t)f32_to_bf16(oacc[dt][4 * g + 2] * inv) |
-                      ((uint32_t)f32_to_bf16(oacc[dt][4 * g + 3] * inv) << 16);
-        *(uint2*)(op + d0) = make_uint2(w0, w1);
-      }
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int d0 = dt * 32 + 8 * r4 + 4 * lhalf;
+          *(uint2*)(op + d0) = make_uint2(pack_bf16x2(oacc[g][dt][4 * r4] * inv, oacc[g][dt][4 * r4 + 1] * inv),
+                                          pack_bf16x2(oacc[g][dt][4 * r4 + 2] * inv, oacc[g][dt][4 * r4 + 3] * inv));
+        }
+    }
   }
 }
 
-// vt[h][d][l] = v[l][h*128 + d] for l < Lk, 0 for Lk <= l < ldvt.
+// vt[h][d][16 g + vt_slot(k)] = v[16 g + k][h*128 + d] for keys < Lk, 0 up to ldvt.
 __global__ __launch_bounds__(256) void transpose_v_kernel(const bf16_t* __restrict__ v, int64_t ldv,
                                                           bf16_t* __restrict__ vt, int Lk, int ldvt) {
   __shared__ bf16_t tile[64][D + 2];
@@ -181,8 +223,9 @@ __global__ __launch_bounds__(256) void transpose_v_kernel(const bf16_t* __restri
     const int l = l0 + r;
     uint32_t w = 0;
     if (l < Lk) w = *(const uint32_t*)(v + (int64_t)l * ldv + h * D + 2 * c2);
-    tile[r][2 * c2] = (bf16_t)(w & 0xffff);
-    tile[r][2 * c2 + 1] = (bf16_t)(w >> 16);
+    const int rs = (r & ~15) | vt_slot(r & 15);
+    tile[rs][2 * c2] = (bf16_t)(w & 0xffff);
+    tile[rs][2 * c2 + 1] = (bf16_t)(w >> 16);
   }
   __syncthreads();
   bf16_t* out = vt + (int64_t)h * D * ldvt + l0;

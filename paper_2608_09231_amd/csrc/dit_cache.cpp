@@ -322,6 +322,7 @@ dit_status validate(const dit_model_config* g, std::string& why) {
     if (g->hidden % 8 || g->mlp_hidden % 8 || g->ctx_dim % 8 || g->in_channels % 8 || g->time_dim % 8)
       return bad("bf16 widths must be multiples of 8");
   } else {
+    if (g->hidden % 4) return bad("f32 hidden must be a multiple of 4");
     if (g->head_dim > 128 || (g->head_dim != 16 && g->head_dim != 32 && g->head_dim != 64 && g->head_dim != 128))
       return bad("f32 path needs head_dim in {16, 32, 64, 128}");
   }

@@ -4,118 +4,196 @@
 // reuse, the Euler update, and the once-per-sample embedding helpers.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace dit {
 namespace {
 
-constexpr int RT = 256;       // threads per row kernel
-constexpr int MAXJ = 32;      // max elements per thread: H <= 8192
-
-// Load one row (H elements) into registers, f32.
-template <typename T>
-__device__ __forceinline__ void load_row(const T* x, int H, float (&v)[MAXJ], int& nj) {
-  nj = (H + RT - 1) / RT;
+// 16-byte chunks of a row: 8 bf16 or 4 f32 values.
+template <typename T> struct Chunk;
+template <> struct Chunk<bf16_t> {
+  static constexpr int E = 8;
+  static __device__ __forceinline__ void load(const bf16_t* p, float (&v)[8]) {
+    const uint4 u = *(const uint4*)p;
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-  for (int j = 0; j < MAXJ; ++j) {
-    const int c = threadIdx.x + RT * j;
-    v[j] = (j < nj && c < H) ? St<T>::ld(x + c) : 0.f;
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
   }
+  static __device__ __forceinline__ void store(bf16_t* p, const float (&v)[8]) {
+    *(uint4*)p = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                            pack_bf16x2(v[6], v[7]));
+  }
+};
+template <> struct Chunk<float> {
+  static constexpr int E = 4;
+  static __device__ __forceinline__ void load(const float* p, float (&v)[4]) {
+    const float4 u = *(const float4*)p;
+    v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+  }
+  static __device__ __forceinline__ void store(float* p, const float (&v)[4]) {
+    *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+  }
+};
+
+// One wave per row: the row lives in registers as MAXC chunks per lane.
+template <typename T, int MAXC>
+struct RowRegs {
+  static constexpr int E = Chunk<T>::E;
+  float v[MAXC][E];
+  int nch;
+  __device__ __forceinline__ void load(const T* x, int H, int lane) {
+    nch = H / E;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = lane + 64 * j;
+      if (c < nch) Chunk<T>::load(x + c * E, v[j]);
+      else
+#pragma unroll
+        for (int e = 0; e < E; ++e) v[j][e] = 0.f;
+    }
+  }
+  // LN statistics over H values (two passes over registers)
+  __device__ __forceinline__ void stats(int H, int lane, float& mean, float& rstd) const {
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j)
+#pragma unroll
+      for (int e = 0; e < E; ++e) s += v[j][e];
+    mean = warp_sum(s) / (float)H;
+    float q = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      if (lane + 64 * j < nch)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const float d = v[j][e] - mean;
+          q += d * d;
+        }
+    }
+    rstd = rsqrtf(warp_sum(q) / (float)H + DIT_LN_EPS);
+  }
+};
+
+__device__ __forceinline__ void load_mod(const float* p, float (&m)[8]) {
+  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+  m[0] = a.x; m[1] = a.y; m[2] = a.z; m[3] = a.w; m[4] = b.x; m[5] = b.y; m[6] = b.z; m[7] = b.w;
+}
+__device__ __forceinline__ void load_mod(const float* p, float (&m)[4]) {
+  const float4 a = *(const float4*)p;
+  m[0] = a.x; m[1] = a.y; m[2] = a.z; m[3] = a.w;
 }
 
-// mean and 1/sqrt(var + eps) of a row held in registers (two passes).
-__device__ __forceinline__ void row_stats(const float (&v)[MAXJ], int nj, int H, float* red,
-                                          float& mean, float& rstd) {
-  float s = 0.f;
-#pragma unroll
-  for (int j = 0; j < MAXJ; ++j) s += v[j];
-  mean = block_sum<RT / 64>(s, red) / (float)H;
-  float q = 0.f;
-#pragma unroll
-  for (int j = 0; j < MAXJ; ++j) {
-    const int c = threadIdx.x + RT * j;
-    const float d = (j < nj && c < H) ? v[j] - mean : 0.f;
-    q += d * d;
-  }
-  const float var = block_sum<RT / 64>(q, red + 8) / (float)H;
-  rstd = rsqrtf(var + DIT_LN_EPS);
-}
-
-template <typename T>
-__global__ __launch_bounds__(RT) void ln_mod_kernel(const T* __restrict__ x, int64_t ldx,
-                                                    T* __restrict__ out, int64_t ldo, int H,
+template <typename T, int MAXC>
+__global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, int64_t ldx,
+                                                    T* __restrict__ out, int64_t ldo, int rows, int H,
                                                     int split, const float* sh0, const float* sc0,
                                                     const float* sh1, const float* sc1) {
-  __shared__ float red[16];
-  const int row = blockIdx.x;
-  float v[MAXJ];
-  int nj;
-  load_row(x + (int64_t)row * ldx, H, v, nj);
+  constexpr int E = Chunk<T>::E;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  RowRegs<T, MAXC> r;
+  r.load(x + (int64_t)row * ldx, H, lane);
   float mean, rstd;
-  row_stats(v, nj, H, red, mean, rstd);
+  r.stats(H, lane, mean, rstd);
   const float* sh = row < split ? sh0 : sh1;
   const float* sc = row < split ? sc0 : sc1;
   T* o = out + (int64_t)row * ldo;
 #pragma unroll
-  for (int j = 0; j < MAXJ; ++j) {
-    const int c = threadIdx.x + RT * j;
-    if (j < nj && c < H) {
-      float y = (v[j] - mean) * rstd;
-      if (sc) y = y * (1.f + sc[c]) + sh[c];
-      St<T>::st(o + c, y);
+  for (int j = 0; j < MAXC; ++j) {
+    const int c = lane + 64 * j;
+    if (c < r.nch) {
+      float y[E];
+      if (sc) {
+        float a[E], b[E];
+        load_mod(sc + c * E, a);
+        load_mod(sh + c * E, b);
+#pragma unroll
+        for (int e = 0; e < E; ++e) y[e] = (r.v[j][e] - mean) * rstd * (1.f + a[e]) + b[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) y[e] = (r.v[j][e] - mean) * rstd;
+      }
+      Chunk<T>::store(o + c * E, y);
     }
   }
 }
 
-// One workgroup per group of IR rows: m = S(LN(h)(1+sc)+sh) (or S(h)),
-// accumulate |m - mp|, |mp|, |m - ml|, |ml|.
-constexpr int IR = 4;
+// Indicator: each wave handles IRW consecutive rows; m = S(LN(h)(1+sc)+sh)
+// (or m = h when sc == nullptr) is written, and |m - mp|, |mp|, |m - ml|,
+// |ml| are summed per lane, then per workgroup (f64 partial 4-vector).
+constexpr int IRW = 4;
+constexpr int IROWS = 4 * IRW;  // rows per workgroup
 
-template <typename T>
-__global__ __launch_bounds__(RT) void indicator_kernel(const T* __restrict__ h, T* __restrict__ m,
+template <typename T, int MAXC>
+__global__ __launch_bounds__(256) void indicator_kernel(const T* __restrict__ h, T* __restrict__ m,
                                                        const T* __restrict__ mp,
                                                        const T* __restrict__ ml, int rows, int H,
                                                        const float* sh, const float* sc,
                                                        double* __restrict__ partials) {
-  __shared__ float red[16];
-  __shared__ float red4[4][RT / 64];
+  constexpr int E = Chunk<T>::E;
+  __shared__ float red[4][4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const bool same = mp == ml;
   float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-  for (int rr = 0; rr < IR; ++rr) {
-    const int row = blockIdx.x * IR + rr;
+  for (int i = 0; i < IRW; ++i) {
+    const int row = (blockIdx.x * 4 + wave) * IRW + i;
     if (row >= rows) break;
     const int64_t base = (int64_t)row * H;
-    float v[MAXJ];
-    int nj;
-    load_row(h + base, H, v, nj);
+    RowRegs<T, MAXC> r;
+    r.load(h + base, H, lane);
     float mean = 0.f, rstd = 1.f;
-    if (sc) row_stats(v, nj, H, red, mean, rstd);
+    if (sc) r.stats(H, lane, mean, rstd);
 #pragma unroll
-    for (int j = 0; j < MAXJ; ++j) {
-      const int c = threadIdx.x + RT * j;
-      if (j < nj && c < H) {
-        float y = sc ? ((v[j] - mean) * rstd) * (1.f + sc[c]) + sh[c] : v[j];
-        y = St<T>::rd(y);
-        St<T>::st(m + base + c, y);
-        if (mp) {
-          const float p = St<T>::ld(mp + base + c);
-          const float l = St<T>::ld(ml + base + c);
-          a0 += fabsf(y - p);
-          a1 += fabsf(p);
-          a2 += fabsf(y - l);
-          a3 += fabsf(l);
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = lane + 64 * j;
+      if (c >= r.nch) continue;
+      float y[E];
+      if (sc) {
+        float a[E], b[E];
+        load_mod(sc + c * E, a);
+        load_mod(sh + c * E, b);
+#pragma unroll
+        for (int e = 0; e < E; ++e) y[e] = St<T>::rd((r.v[j][e] - mean) * rstd * (1.f + a[e]) + b[e]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) y[e] = r.v[j][e];
+      }
+      Chunk<T>::store(m + base + c * E, y);
+      if (mp) {
+        float p[E];
+        Chunk<T>::load(mp + base + c * E, p);
+        float l[E];
+        if (same) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) l[e] = p[e];
+        } else {
+          Chunk<T>::load(ml + base + c * E, l);
+        }
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          a0 += fabsf(y[e] - p[e]);
+          a1 += fabsf(p[e]);
+          a2 += fabsf(y[e] - l[e]);
+          a3 += fabsf(l[e]);
         }
       }
     }
   }
   if (!partials) return;
   a0 = warp_sum(a0); a1 = warp_sum(a1); a2 = warp_sum(a2); a3 = warp_sum(a3);
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) { red4[0][w] = a0; red4[1][w] = a1; red4[2][w] = a2; red4[3][w] = a3; }
+  if (lane == 0) { red[wave][0] = a0; red[wave][1] = a1; red[wave][2] = a2; red[wave][3] = a3; }
   __syncthreads();
   if (threadIdx.x < 4) {
     double s = 0.0;
-    for (int i = 0; i < RT / 64; ++i) s += (double)red4[threadIdx.x][i];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) s += (double)red[w][threadIdx.x];
     partials[(int64_t)blockIdx.x * 4 + threadIdx.x] = s;
   }
 }
@@ -231,27 +309,43 @@ inline int grid_for(int64_t n, int bs) {
 
 }  // namespace
 
+template <typename T, typename F>
+hipError_t dispatch_maxc(int H, F f) {
+  constexpr int E = Chunk<T>::E;
+  const int per_lane = (H / E + 63) / 64;
+  if (per_lane <= 2) return f(std::integral_constant<int, 2>());
+  if (per_lane <= 4) return f(std::integral_constant<int, 4>());
+  if (per_lane <= 8) return f(std::integral_constant<int, 8>());
+  if (per_lane <= 16) return f(std::integral_constant<int, 16>());
+  if (per_lane <= 32) return f(std::integral_constant<int, 32>());
+  return hipErrorInvalidValue;
+}
+
 template <typename T>
 hipError_t launch_ln_mod(const T* x, int64_t ldx, T* out, int64_t ldo, int rows, int H, int split,
                          const float* sh0, const float* sc0, const float* sh1, const float* sc1,
                          hipStream_t s) {
-  if (H > RT * MAXJ) return hipErrorInvalidValue;
+  if (H % Chunk<T>::E) return hipErrorInvalidValue;
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(ln_mod_kernel<T>, dim3(rows), dim3(RT), 0, s, x, ldx, out, ldo, H, split, sh0,
-                     sc0, sh1, sc1);
-  return hipGetLastError();
+  return dispatch_maxc<T>(H, [&](auto mc) {
+    hipLaunchKernelGGL((ln_mod_kernel<T, decltype(mc)::value>), dim3((rows + 3) / 4), dim3(256), 0, s, x,
+                       ldx, out, ldo, rows, H, split, sh0, sc0, sh1, sc1);
+    return hipGetLastError();
+  });
 }
 
 template <typename T>
 hipError_t launch_indicator(const T* h, T* m_out, const T* m_prev, const T* m_last, int rows, int H,
                             const float* sh, const float* sc, double* partials, int* n_partials,
                             hipStream_t s) {
-  if (H > RT * MAXJ) return hipErrorInvalidValue;
-  const int nb = (rows + IR - 1) / IR;
+  if (H % Chunk<T>::E) return hipErrorInvalidValue;
+  const int nb = (rows + IROWS - 1) / IROWS;
   if (n_partials) *n_partials = nb;
-  hipLaunchKernelGGL(indicator_kernel<T>, dim3(nb), dim3(RT), 0, s, h, m_out, m_prev, m_last, rows,
-                     H, sh, sc, partials);
-  return hipGetLastError();
+  return dispatch_maxc<T>(H, [&](auto mc) {
+    hipLaunchKernelGGL((indicator_kernel<T, decltype(mc)::value>), dim3(nb), dim3(256), 0, s, h, m_out,
+                       m_prev, m_last, rows, H, sh, sc, partials);
+    return hipGetLastError();
+  });
 }
 
 hipError_t launch_reduce_partials(const double* partials, int n, double* out, hipStream_t s) {
