@@ -105,6 +105,27 @@ def cpu_baseline(w, budget_s=40.0):
     }
 
 
+def gemm_traffic(workload):
+    """HBM-side bytes per GEMM launch from the committed rocprofv3 counter
+    summary, or None when it does not cover this workload or the GEMM
+    source changed since the counters were taken."""
+    import hashlib
+    import re
+
+    path = os.path.join(ROOT, "profiles", f"gemm_bf16_{workload}_hbm_traffic.md")
+    src = os.path.join(ROOT, "paper_2608_09231_amd", "csrc", "gemm_bf16.hip")
+    try:
+        txt = open(path).read()
+        m = re.search(r"```json\n(.*?)\n```", txt, flags=re.S)
+        data = json.loads(m.group(1))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except (OSError, AttributeError, ValueError):
+        return None
+    if data.get("gemm_source_sha256_16") != sha:
+        return None
+    return data["traffic_bytes_per_launch"]
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,6 +134,8 @@ def main():
     ap.add_argument("--workload", default="flux1024")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one plain 256 MiB device-to-device copy first (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the sampler has no multi-GPU path "
@@ -134,6 +157,15 @@ def main():
     text = synth.make_text(cfg, w.seed)
     gate = synth.make_gate_blob(w.gate_widths, w.seed, w.gate_std)
     log(f"[bench] inputs ready in {time.time() - t0:.1f} s; uploading")
+    if args.copy_calibration:
+        n = 64 << 20                     # 64 Mi float32 = 256 MiB read + 256 MiB written
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy: {n * 4} bytes read, {n * 4} bytes written")
+        del src, dst
     stream = torch.cuda.current_stream()
     h = binding.DitCache(cfg, weights.blob, stream)
     del weights
@@ -195,7 +227,8 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": gemm_tflops / PEAK_BF16_TFLOPS,
-            "traffic": None,
+            "traffic": gemm_traffic(cfg.name),
+            "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "avg_launch_us": ms["gemm"] * 1e3 / launches,
             "flops_per_launch": work["gemm"] / launches,
         },
