@@ -68,14 +68,18 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 }
 
 // GELU, tanh form: 0.5 x (1 + tanh(u)) = x * sigmoid(2u), u = sqrt(2/pi)(x + 0.044715 x^3).
-// The sigmoid form has no cancellation for large negative x.
+// The sigmoid form has no cancellation for large negative x.  exp via the
+// hardware base-2 exponential and a hardware reciprocal (about 1 ulp each,
+// far below the bf16 rounding of the stored result).
 __device__ __forceinline__ float gelu_tanh_f(float x) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  const float u = k0 * (x + 0.044715f * x * x * x);
-  return x / (1.f + expf(-2.f * u));
+  const float k0 = 0.7978845608028654f * -2.f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  const float e = __builtin_amdgcn_exp2f(k0 * (x + 0.044715f * x * x * x));
+  return x * __builtin_amdgcn_rcpf(1.f + e);
 }
 
-__device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
+__device__ __forceinline__ float silu_f(float x) {
+  return x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
+}
 
 #define DIT_LN_EPS 1e-6f
 #define DIT_RMS_EPS 1e-6f

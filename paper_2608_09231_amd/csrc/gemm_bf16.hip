@@ -4,12 +4,15 @@
 // A [M,K] and W [N,K] are both K-contiguous (W in nn.Linear [out,in]
 // layout), so every MFMA operand is a 16-byte run of K.  Tiles of BM x BN
 // are staged through LDS in BK = 64 slices, double-buffered, with the
-// 16-byte chunks of each 128-byte row XOR-swizzled by (row & 7) so that
-// the fragment reads of 32 consecutive rows hit distinct banks.  Four waves
+// 16-byte chunks of each 128-byte row XOR-swizzled by ((row >> 1) & 7): two
+// consecutive 128-byte rows fill one 256-byte bank cycle, so the fragment
+// reads of 16 consecutive rows hit 16 distinct 16-byte bank groups.  Four waves
 // per workgroup, each owning a WM x WN sub-tile of 32x32 MFMA tiles.
 // Workgroups are remapped so that each of the 8 XCDs walks a contiguous,
 // M-grouped range of tiles (its own L2 sees the shared A rows / W columns).
 #include <stdlib.h>
+
+#include <utility>
 
 #include "common.h"
 #include "kernels.h"
@@ -164,12 +167,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(Batch b) {
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) {
       const int q = tid + 256 * i, row = q >> 3, kc = q & 7;
-      *(uint4*)(sA + row * BK + ((kc ^ (row & 7)) << 3)) = ra[i];
+      *(uint4*)(sA + row * BK + ((kc ^ ((row >> 1) & 7)) << 3)) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < B_LD; ++i) {
       const int q = tid + 256 * i, row = q >> 3, kc = q & 7;
-      *(uint4*)(sB + row * BK + ((kc ^ (row & 7)) << 3)) = rb[i];
+      *(uint4*)(sB + row * BK + ((kc ^ ((row >> 1) & 7)) << 3)) = rb[i];
     }
   };
 
@@ -198,13 +201,13 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(Batch b) {
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = wm * WM + i * 32 + lrow;
-        uint4 v = *(const uint4*)(sA + row * BK + ((kc ^ (row & 7)) << 3));
+        uint4 v = *(const uint4*)(sA + row * BK + ((kc ^ ((row >> 1) & 7)) << 3));
         af[i] = __builtin_bit_cast(bf16x8_t, v);
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int row = wn * WN + j * 32 + lrow;
-        uint4 v = *(const uint4*)(sB + row * BK + ((kc ^ (row & 7)) << 3));
+        uint4 v = *(const uint4*)(sB + row * BK + ((kc ^ ((row >> 1) & 7)) << 3));
         bfr[j] = __builtin_bit_cast(bf16x8_t, v);
       }
 #pragma unroll
@@ -220,24 +223,173 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(Batch b) {
   epilogue<TM, TN, WM, WN>(P, acc, m0, n0, wm, wn, lrow, lhalf);
 }
 
+// LDS-staged epilogue for waves that own 128 output columns (WN == 128).
+// Per 32-row slab: the raw f32 accumulators go to this wave's 16 KB of LDS
+// (columns XOR 32 on rows with bit 2 set, so the two lane halves of a write
+// hit different banks); then lane l handles rows l/16 + 4p (p = 0..7) and
+// columns 4(l%16) + [0,4) and 64 + 4(l%16) + [0,4): bias, per-head RMS (a
+// head is the 16 lanes of one row: 4 shuffles), GELU / SiLU, gated
+// residual, and 8-byte stores that coalesce to 128 bytes per row.
+// Requires N % 8 == 0, gelu_from and gap_at multiples of 4.
+struct EpiLds {
+  const Prob& P;
+  int m_base, ncol0, cq, rq, lrow, lhalf;
+  bool f32out, gated, silu, rms;
+  float bv[2][4], gv[2][4];
+  int col[2];
+  bool ok[2], gl[2];
+  float* slab;
+
+  __device__ __forceinline__ EpiLds(const Prob& P_, int m_base_, int ncol0_, int lrow_, int lhalf_, float* slab_)
+      : P(P_), m_base(m_base_), ncol0(ncol0_), lrow(lrow_), lhalf(lhalf_), slab(slab_) {
+    const int lane = lhalf * 32 + lrow;
+    cq = lane & 15;
+    rq = lane >> 4;
+    f32out = P.flags & DIT_EPI_F32;
+    gated = P.flags & DIT_EPI_GATED_RES;
+    silu = P.flags & DIT_EPI_SILU;
+    rms = ncol0 < P.rms_cols;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int n = ncol0 + 64 * hh + 4 * cq;
+      ok[hh] = n < P.N;
+      gl[hh] = n >= P.gelu_from;
+      col[hh] = n + (n >= P.gap_at ? P.gap : 0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        bv[hh][e] = (P.bias && ok[hh]) ? bf16_to_f32(P.bias[n + e]) : 0.f;
+        gv[hh][e] = (gated && ok[hh]) ? P.gate[n + e] : 0.f;
+      }
+    }
+  }
+
+  // one 32-row slab: accumulators -> LDS -> 8-column row segments -> global
+  __device__ __forceinline__ void slab_pass(const f32x16_t (&a)[4], int i) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 8 * (r >> 2) + 4 * lhalf + (r & 3);
+        const int c = (j * 32 + lrow) ^ (((row >> 2) & 1) << 5);
+        slab[row * 128 + c] = a[j][r];
+      }
+    __builtin_amdgcn_s_waitcnt(0);
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      const int row = rq + 4 * p;
+      const int sw = ((row >> 2) & 1) << 5;
+      float v[2][4];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const float4 t = *(const float4*)(slab + row * 128 + ((64 * hh + 4 * cq) ^ sw));
+        v[hh][0] = t.x + bv[hh][0]; v[hh][1] = t.y + bv[hh][1];
+        v[hh][2] = t.z + bv[hh][2]; v[hh][3] = t.w + bv[hh][3];
+      }
+      if (rms) {
+        float ss = 0.f;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) ss += v[hh][e] * v[hh][e];
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) ss += __shfl_xor(ss, o, 64);
+        const float sc = rsqrtf(ss * (1.f / 128.f) + DIT_RMS_EPS);
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[hh][e] *= sc;
+      }
+      const int m = m_base + i * 32 + row;
+      if (m < P.M) {
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          if (!ok[hh]) continue;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (gl[hh]) v[hh][e] = gelu_tanh_f(v[hh][e]);
+            if (silu) v[hh][e] = silu_f(v[hh][e]);
+          }
+          if (f32out) {
+            *(float4*)((float*)P.C + (int64_t)m * P.ldc + col[hh]) =
+                make_float4(v[hh][0], v[hh][1], v[hh][2], v[hh][3]);
+          } else {
+            bf16_t* c = (bf16_t*)P.C + (int64_t)m * P.ldc + col[hh];
+            if (gated) {
+              const uint2 old = *(const uint2*)c;
+              v[hh][0] = __uint_as_float(old.x << 16) + gv[hh][0] * v[hh][0];
+              v[hh][1] = __uint_as_float(old.x & 0xffff0000u) + gv[hh][1] * v[hh][1];
+              v[hh][2] = __uint_as_float(old.y << 16) + gv[hh][2] * v[hh][2];
+              v[hh][3] = __uint_as_float(old.y & 0xffff0000u) + gv[hh][3] * v[hh][3];
+            }
+            *(uint2*)c = make_uint2(pack_bf16x2(v[hh][0], v[hh][1]), pack_bf16x2(v[hh][2], v[hh][3]));
+          }
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+  }
+};
+
+// LDS-staged epilogue for waves that own 128 output columns (WN == 128).
+// Per 32-row slab: the raw f32 accumulators go to this wave's 16 KB of LDS
+// (columns XOR 32 on rows with bit 2 set, so the two lane halves of a write
+// hit different banks); then lane l handles rows l/16 + 4p (p = 0..7) and
+// columns 4(l%16) + [0,4) and 64 + 4(l%16) + [0,4): bias, per-head RMS (a
+// head is the 16 lanes of one row: 4 shuffles), GELU / SiLU, gated
+// residual, and 8-byte stores that coalesce to 128 bytes per row.  Each slab
+// index is a compile-time constant so the accumulators stay in registers.
+// Requires N % 8 == 0, gelu_from and gap_at multiples of 4.
+template <int TM, size_t... Is>
+__device__ __forceinline__ void epilogue_lds_impl(EpiLds& e, f32x16_t (&acc)[TM][4], std::index_sequence<Is...>) {
+  (e.slab_pass(acc[Is], (int)Is), ...);
+}
+
+template <int TM>
+__device__ __forceinline__ void epilogue_lds(const Prob& P, f32x16_t (&acc)[TM][4], int m0, int n0, int wm,
+                                             int wn, int lrow, int lhalf, float* slab) {
+  EpiLds e(P, m0 + wm * TM * 32, n0 + wn * 128, lrow, lhalf, slab);
+  epilogue_lds_impl<TM>(e, acc, std::make_index_sequence<TM>{});
+}
+
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
-// Direct-to-LDS variant (K % 64 == 0): tiles are copied by
-// global_load_lds_dwordx4 (64 lanes x 16 bytes into a contiguous 1 KB per
-// instruction), so no staging registers are needed and a wave can hold a
-// 128 x 128 accumulator block.  The per-lane source chunk realises the same
-// XOR swizzle as the register-staged kernel.
-template <int BM, int BN, int WGM, int WGN>
+// A DMA config uses the LDS-staged epilogue when its waves own 128 columns
+// and its LDS holds one 32 x 128 f32 slab per wave; the host only picks such
+// a config for problems that meet the epilogue's alignment conditions.
+template <int WN, int NW, int LDS_BYTES>
+constexpr bool kLdsEpilogue = WN == 128 && LDS_BYTES >= NW * 32 * 128 * 4;
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt[3:0] | expcnt[6:4] = 7 | lgkmcnt[11:8] = 15 | vmcnt[5:4] at [15:14]).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Direct-to-LDS pipeline (K % BK == 0): BK-deep slices of A and W are copied
+// by global_load_lds_dwordx4 (64 lanes x 16 bytes into a contiguous 1 KB per
+// instruction: no staging registers), STAGES slices in flight.  A slice row
+// has CPR = BK/8 chunks of 16 bytes; RPB = 256/(2 BK) rows share one 256-byte
+// bank cycle, and chunk c of row r is stored at c ^ ((r / RPB) % CPR), so the
+// fragment reads of 16 consecutive rows hit 16 distinct bank groups.  The
+// per-lane source chunk of each copy realises the same swizzle.
+template <int BM, int BN, int WGM, int WGN, int BK_, int STAGES>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) {
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int NW = WGM * WGN;
-  constexpr int A_INS = BM / (8 * NW), B_INS = BN / (8 * NW);  // 1 KB copies per wave per slice
-  constexpr int STAGE = (BM + BN) * BK * 2;                   // bytes
-  static_assert(A_INS >= 1 && B_INS >= 1 && A_INS * 8 * NW == BM && B_INS * 8 * NW == BN, "tile");
+  constexpr int CPR = BK_ / 8, RPB = 256 / (2 * BK_);
+  constexpr int ROWS_PER_INS = 64 / CPR;
+  constexpr int A_INS = BM / (ROWS_PER_INS * NW), B_INS = BN / (ROWS_PER_INS * NW);
+  constexpr int INS = A_INS + B_INS;                 // copies per wave per slice
+  constexpr int STAGE = (BM + BN) * BK_ * 2;         // bytes
+  static_assert(A_INS >= 1 && B_INS >= 1 && A_INS * ROWS_PER_INS * NW == BM &&
+                    B_INS * ROWS_PER_INS * NW == BN, "tile");
+  static_assert(STAGES >= 2 && (STAGES - 2) * INS < 64, "stages");
 
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
   if ((int)blockIdx.x >= b.total) return;
   int lt = xcd_remap(blockIdx.x, b.total);
@@ -263,21 +415,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
   uint32_t aoff[A_INS], boff[B_INS];
 #pragma unroll
   for (int j = 0; j < A_INS; ++j) {
-    const int row = 8 * (wave * A_INS + j) + (lane >> 3);
-    const int c = (lane & 7) ^ (row & 7);
+    const int row = ROWS_PER_INS * (wave * A_INS + j) + lane / CPR;
+    const int c = (lane % CPR) ^ ((row / RPB) % CPR);
     aoff[j] = (uint32_t)min(m0 + row, P.M - 1) * (uint32_t)P.lda + c * 8;
   }
 #pragma unroll
   for (int j = 0; j < B_INS; ++j) {
-    const int row = 8 * (wave * B_INS + j) + (lane >> 3);
-    const int c = (lane & 7) ^ (row & 7);
+    const int row = ROWS_PER_INS * (wave * B_INS + j) + lane / CPR;
+    const int c = (lane % CPR) ^ ((row / RPB) % CPR);
     boff[j] = (uint32_t)min(n0 + row, P.N - 1) * (uint32_t)P.ldw + c * 8;
   }
-  auto issue = [&](int k0, int st) {
-    char* sA = smem + st * STAGE;
-    char* sB = sA + BM * BK * 2;
-    const bf16_t* Ab = P.A + k0;
-    const bf16_t* Bb = P.W + k0;
+  auto issue = [&](int kt) {
+    char* sA = smem + (kt % STAGES) * STAGE;
+    char* sB = sA + BM * BK_ * 2;
+    const bf16_t* Ab = P.A + kt * BK_;
+    const bf16_t* Bb = P.W + kt * BK_;
 #pragma unroll
     for (int j = 0; j < A_INS; ++j)
       __builtin_amdgcn_global_load_lds((glb_void_t*)(Ab + aoff[j]), (lds_void_t*)(sA + (wave * A_INS + j) * 1024), 16, 0, 0);
@@ -294,28 +446,32 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int nk = P.K / BK;
-  issue(0, 0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  const int nk = P.K / BK_;
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s);
 
   for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) issue((kt + 1) * BK, (kt + 1) & 1);
-    const char* sA = smem + (kt & 1) * STAGE;
-    const char* sB = sA + BM * BK * 2;
+    // slice kt must have landed: later slices may stay in flight
+    if (nk - 1 - kt >= STAGES - 2) wait_vmcnt<(STAGES - 2) * INS>();
+    else __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // every wave's copies of slice kt are in; slice kt-1 is no longer read
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+    const char* sA = smem + (kt % STAGES) * STAGE;
+    const char* sB = sA + BM * BK_ * 2;
 #pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
+    for (int s = 0; s < BK_ / 16; ++s) {
       const int kc = 2 * s + lhalf;
       bf16x8_t af[TM], bfr[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = wm * WM + i * 32 + lrow;
-        af[i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sA + row * 128 + ((kc ^ (row & 7)) << 4)));
+        af[i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sA + row * (2 * BK_) + ((kc ^ ((row / RPB) % CPR)) << 4)));
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int row = wn * WN + j * 32 + lrow;
-        bfr[j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sB + row * 128 + ((kc ^ (row & 7)) << 4)));
+        bfr[j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sB + row * (2 * BK_) + ((kc ^ ((row / RPB) % CPR)) << 4)));
       }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
@@ -323,14 +479,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
   }
-  epilogue<TM, TN, WM, WN>(P, acc, m0, n0, wm, wn, lrow, lhalf);
+  __syncthreads();  // all waves are done with the slices before the epilogue reuses LDS
+  if constexpr (kLdsEpilogue<WN, NW, STAGES * STAGE>) {
+    float* slab = (float*)smem + wave * (32 * 128);
+    epilogue_lds<TM>(P, acc, m0, n0, wm, wn, lrow, lhalf, slab);
+  } else {
+    epilogue<TM, TN, WM, WN>(P, acc, m0, n0, wm, wn, lrow, lhalf);
+  }
 }
 
 struct Cfg {
-  int bm, bn, wn, wg_per_cu, threads;
+  int bm, bn, wn, wg_per_cu, threads, bk;
+  bool lds_epi;
   float eff;
   bool dma;
   void (*fn)(Batch);
@@ -339,15 +500,22 @@ struct Cfg {
 // eff: relative MFMA efficiency of a full tile (measured ordering); the
 // chooser minimises rounds x per-round work / eff over the configs a
 // problem admits.
+#define DIT_DMA_CFG(BM, BN, WGM, WGN, BK_, ST, WPC, EFF)                                      \
+  {BM, BN, BN / WGN, WPC, 64 * WGM * WGN, BK_,                                                 \
+   kLdsEpilogue<BN / WGN, WGM * WGN, ST * (BM + BN) * BK_ * 2>, EFF, true,                     \
+   gemm_bf16_dma_kernel<BM, BN, WGM, WGN, BK_, ST>}
 const Cfg kCfgs[] = {
-    {256, 256, 128, 1, 512, 1.00f, true, gemm_bf16_dma_kernel<256, 256, 4, 2>},
-    {256, 128, 128, 1, 256, 0.72f, true, gemm_bf16_dma_kernel<256, 128, 4, 1>},
-    {128, 128, 128, 2, 256, 0.85f, true, gemm_bf16_dma_kernel<128, 128, 4, 1>},
-    {32, 256, 64, 2, 256, 0.45f, true, gemm_bf16_dma_kernel<32, 256, 1, 4>},
-    {256, 128, 128, 1, 256, 0.60f, false, gemm_bf16_kernel<256, 128, 4, 1>},
-    {128, 128, 128, 2, 256, 0.55f, false, gemm_bf16_kernel<128, 128, 4, 1>},
-    {32, 256, 64, 2, 256, 0.30f, false, gemm_bf16_kernel<32, 256, 1, 4>},
+    DIT_DMA_CFG(256, 256, 4, 2, 64, 2, 1, 1.00f),
+    DIT_DMA_CFG(256, 256, 4, 2, 32, 4, 1, 0.95f),
+    DIT_DMA_CFG(256, 256, 2, 2, 64, 2, 1, 0.99f),
+    DIT_DMA_CFG(256, 128, 4, 1, 64, 2, 1, 0.72f),
+    DIT_DMA_CFG(128, 128, 4, 1, 64, 2, 2, 0.85f),
+    DIT_DMA_CFG(32, 256, 1, 4, 64, 2, 2, 0.45f),
+    {256, 128, 128, 1, 256, 64, false, 0.60f, false, gemm_bf16_kernel<256, 128, 4, 1>},
+    {128, 128, 128, 2, 256, 64, false, 0.55f, false, gemm_bf16_kernel<128, 128, 4, 1>},
+    {32, 256, 64, 2, 256, 64, false, 0.30f, false, gemm_bf16_kernel<32, 256, 1, 4>},
 };
+#undef DIT_DMA_CFG
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 Prob make_prob(const GemmArgs& g, int bm, int bn) {
@@ -374,19 +542,32 @@ int forced_cfg() {
 }
 
 int pick_cfg(const GemmArgs* g, int n, int n_cu) {
-  bool rms = false, k64 = true;
+  bool rms = false, aligned = true;
   for (int i = 0; i < n; ++i) {
     rms |= g[i].rms_cols > 0;
-    k64 &= (g[i].K % BK) == 0 && (g[i].lda % 8) == 0 && (g[i].ldw % 8) == 0;
+    aligned &= (g[i].lda % 8) == 0 && (g[i].ldw % 8) == 0;
   }
+  bool epi_ok = true;  // conditions of the LDS-staged epilogue
+  for (int i = 0; i < n; ++i) {
+    epi_ok &= (g[i].N % 8) == 0 && (g[i].ldc % 4) == 0;
+    epi_ok &= g[i].gelu_from >= g[i].N || (g[i].gelu_from % 4) == 0;
+    epi_ok &= g[i].gap == 0 || ((g[i].gap_at | g[i].gap) % 4) == 0;
+  }
+  auto admits = [&](const Cfg& k) {
+    if (rms && k.wn % 128) return false;
+    if (!k.dma) return true;
+    if (!aligned || (k.lds_epi && !epi_ok)) return false;
+    for (int i = 0; i < n; ++i)
+      if (g[i].K % k.bk) return false;
+    return true;
+  };
   const int f = forced_cfg();
-  if (f >= 0 && f < kNumCfgs && (k64 || !kCfgs[f].dma) && (!rms || kCfgs[f].wn % 128 == 0)) return f;
+  if (f >= 0 && f < kNumCfgs && admits(kCfgs[f])) return f;
   int best = -1;
   double best_t = 1e300;
   for (int c = 0; c < kNumCfgs; ++c) {
     const Cfg& k = kCfgs[c];
-    if (k.dma && !k64) continue;
-    if (rms && k.wn % 128) continue;
+    if (!admits(k)) continue;
     long tiles = 0;
     for (int i = 0; i < n; ++i)
       tiles += (long)((g[i].M + k.bm - 1) / k.bm) * ((g[i].N + k.bn - 1) / k.bn);
