@@ -58,16 +58,24 @@ typedef struct dit_gemm_desc {
 
 dit_status dit_gemm_bf16(const dit_gemm_desc* d, void* hip_stream);
 
+/* Attention flags. */
+enum {
+  /* The caller guarantees |q . k| <= 128 per head (e.g. q and k RMS-normalised
+   * with unit gain), so every logit is at most sqrt(128) and a fixed shift
+   * replaces the running maximum of the softmax (same result). */
+  DIT_ATTN_BOUNDED_LOGITS = 1
+};
+
 /* o = softmax(q k^T / sqrt(128)) v per head (non-causal), bf16 in and out,
  * f32 softmax and accumulation on MFMA.  q [Lq, heads*128] (row stride
  * ldq), k and v [Lk, heads*128] (ldk, ldv), o [Lq, heads*128] (ldo);
- * head h occupies columns [128h, 128h + 128).  vt_ws is a device
- * workspace of heads * 128 * round_up(Lk, 64) bf16 elements that receives
- * v transposed per head.  Errors: DIT_EINVAL, DIT_ESHAPE (Lq, Lk < 1),
- * DIT_EHIP. */
+ * head h occupies columns [128h, 128h + 128).  flags: 0 or
+ * DIT_ATTN_BOUNDED_LOGITS.  vt_ws is a device workspace of heads * 128 *
+ * round_up(Lk, 64) bf16 elements that receives v transposed per head.
+ * Errors: DIT_EINVAL, DIT_ESHAPE (Lq, Lk < 1), DIT_EHIP. */
 dit_status dit_attention_bf16(const void* q, int64_t ldq, const void* k, int64_t ldk,
                               const void* v, int64_t ldv, void* o, int64_t ldo,
-                              int32_t Lq, int32_t Lk, int32_t heads, void* vt_ws,
+                              int32_t Lq, int32_t Lk, int32_t heads, int32_t flags, void* vt_ws,
                               void* hip_stream);
 
 #ifdef __cplusplus

@@ -95,7 +95,7 @@ def load(path: str = LIB_PATH):
     lib.dit_cache_reset_stats.argtypes = [vp]
     lib.dit_gemm_bf16.argtypes = [C.POINTER(GemmDescC), vp]
     lib.dit_attention_bf16.argtypes = [vp, C.c_int64, vp, C.c_int64, vp, C.c_int64, vp, C.c_int64,
-                                       C.c_int32, C.c_int32, C.c_int32, vp, vp]
+                                       C.c_int32, C.c_int32, C.c_int32, C.c_int32, vp, vp]
     for n in EXPORTS:
         f = getattr(lib, n)
         if n not in ("dit_cache_destroy", "dit_cache_last_error"):
@@ -225,8 +225,11 @@ def gemm_bf16(A, W, bias, Cout, *, M, N, K, lda=None, ldw=None, ldc=None, flags=
     _check(st, None)
 
 
-def attention_bf16(q, k, v, o, *, Lq, Lk, heads, ldq, ldk, ldv, ldo, vt_ws, stream=None):
+ATTN_BOUNDED_LOGITS = 1
+
+
+def attention_bf16(q, k, v, o, *, Lq, Lk, heads, ldq, ldk, ldv, ldo, vt_ws, flags=0, stream=None):
     lib = load()
     st = lib.dit_attention_bf16(q.data_ptr(), ldq, k.data_ptr(), ldk, v.data_ptr(), ldv,
-                                o.data_ptr(), ldo, Lq, Lk, heads, vt_ws.data_ptr(), _stream_ptr(stream))
+                                o.data_ptr(), ldo, Lq, Lk, heads, flags, vt_ws.data_ptr(), _stream_ptr(stream))
     _check(st, None)

@@ -245,8 +245,9 @@ dit_status attention(dit_cache* c, const void* q, int64_t ldq, const void* k, in
       HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt_ws, Lk, heads, c->stream));
     }
     Scope s(c, DIT_K_ATTN, flops);
+    // q and k leave the projection through a unit-gain RMS norm: bounded logits
     HIPCK(dit::launch_flash_attn_bf16(q, ldq, k, ldk, vt_ws, (int)rup(Lk, 64), o, ldo, Lq, Lk, heads,
-                                      c->stream));
+                                      true, c->stream));
   } else {
     Scope s(c, DIT_K_ATTN, flops);
     HIPCK(dit::launch_attn_f32((const float*)q, ldq, (const float*)k, ldk, (const float*)v, ldv,
@@ -954,16 +955,18 @@ dit_status dit_gemm_bf16(const dit_gemm_desc* d, void* hip_stream) {
 }
 
 dit_status dit_attention_bf16(const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v, int64_t ldv,
-                              void* o, int64_t ldo, int32_t Lq, int32_t Lk, int32_t heads, void* vt_ws,
-                              void* hip_stream) {
+                              void* o, int64_t ldo, int32_t Lq, int32_t Lk, int32_t heads, int32_t flags,
+                              void* vt_ws, void* hip_stream) {
   dit_cache* c = nullptr;
   if (!q || !k || !v || !o || !vt_ws) return fail(c, DIT_EINVAL, "null argument");
   if (Lq < 1 || Lk < 1 || heads < 1) return fail(c, DIT_ESHAPE, "bad attention shape");
+  if (flags & ~DIT_ATTN_BOUNDED_LOGITS) return fail(c, DIT_EINVAL, "bad attention flags");
   if (ldq < heads * 128 || ldk < heads * 128 || ldv < heads * 128 || ldo < heads * 128)
     return fail(c, DIT_ESHAPE, "row stride smaller than heads*128");
   hipStream_t s = (hipStream_t)hip_stream;
   HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt_ws, Lk, heads, s));
-  HIPCK(dit::launch_flash_attn_bf16(q, ldq, k, ldk, vt_ws, (int)rup(Lk, 64), o, ldo, Lq, Lk, heads, s));
+  HIPCK(dit::launch_flash_attn_bf16(q, ldq, k, ldk, vt_ws, (int)rup(Lk, 64), o, ldo, Lq, Lk, heads,
+                                    (flags & DIT_ATTN_BOUNDED_LOGITS) != 0, s));
   HIPCK(hipStreamSynchronize(s));
   return DIT_OK;
 }

@@ -33,7 +33,7 @@ hipError_t launch_transpose_v_bf16(const void* v, int64_t ldv, void* vt, int Lk,
                                    hipStream_t s);
 hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int64_t ldk,
                                   const void* vt, int ldvt, void* o, int64_t ldo, int Lq,
-                                  int Lk, int heads, hipStream_t s);
+                                  int Lk, int heads, bool bounded_logits, hipStream_t s);
 // f32 attention, head_dim <= 128 (multiple of 4).
 hipError_t launch_attn_f32(const float* q, int64_t ldq, const float* k, int64_t ldk,
                            const float* v, int64_t ldv, float* o, int64_t ldo, int Lq, int Lk,

@@ -148,3 +148,28 @@ def test_gemm_flux1024_single_block_shape_sampled():
         assert_bf16_close(got[r, :2 * H], qk, frac_exact=0.8)
         assert_bf16_close(got[r, 2 * H:3 * H], round_bf16(y[2 * H:3 * H]), frac_exact=0.8)
         assert_bf16_close(got[r, 4 * H:], round_bf16(dit.gelu_tanh(y[3 * H:])), frac_exact=0.8)
+
+
+@pytest.mark.parametrize("L,heads", [(4608, 24), (333, 2)])
+def test_attention_bounded_logits_rms_normalised(L, heads):
+    """The sampler's path: q and k leave a unit-gain RMS norm, so the kernel
+    may replace the running max by a fixed shift (DIT_ATTN_BOUNDED_LOGITS)."""
+    torch = torch_cuda()
+    H = heads * 128
+    def mk(n, norm):
+        x = RNG.standard_normal((n, H)) * 3.0
+        if norm:
+            x = dit.rms_heads(x, heads, 128)
+        b = bf16_bits(x)
+        return b, bits_to_f64(b)
+    q_b, q = mk(L, True)
+    k_b, k = mk(L, True)
+    v_b, v = mk(L, False)
+    o = torch.zeros((L, H), dtype=torch.int16, device="cuda")
+    ws = torch.zeros(heads * 128 * ((L + 63) // 64 * 64), dtype=torch.int16, device="cuda")
+    binding.attention_bf16(dev(torch, q_b), dev(torch, k_b), dev(torch, v_b), o, Lq=L, Lk=L, heads=heads,
+                           ldq=H, ldk=H, ldv=H, ldo=H, vt_ws=ws, flags=binding.ATTN_BOUNDED_LOGITS)
+    got = host_bf16(o)
+    rows = np.sort(RNG.choice(L, min(L, 64), replace=False))
+    ref = round_bf16(dit.attention(q[rows], k, v, heads, 128))
+    assert rel_l2(got[rows], ref) < 4e-3
