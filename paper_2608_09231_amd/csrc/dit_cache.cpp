@@ -80,7 +80,6 @@ struct dit_cache {
   void* A = nullptr;       // [L, H] modulated block input
   void* Y = nullptr;       // [L, 4H+F]: q | k | v | attn out | mlp hidden
   void* vt = nullptr;      // bf16 [heads, 128, round_up(L, 64)]
-  void* hout = nullptr;    // [N, H]
   void* yf = nullptr;      // [N, H] final-layer input
   float* vel = nullptr;    // f32 [nb, N, C]
   void* txt = nullptr;     // [nb, Nt, H]
@@ -351,7 +350,6 @@ dit_status alloc_workspace(dit_cache* c) {
   TRY(dalloc(c, &c->A, (size_t)L * H * e));
   TRY(dalloc(c, &c->Y, (size_t)L * c->ldY * e));
   if (c->bf16) TRY(dalloc(c, &c->vt, (size_t)c->cfg.heads * 128 * rup(L, 64) * 2));
-  TRY(dalloc(c, &c->hout, (size_t)N * H * e));
   TRY(dalloc(c, &c->yf, (size_t)N * H * e));
   TRY(dalloc(c, &c->vel, (size_t)c->nb * N * c->C * 4));
   TRY(dalloc(c, &c->txt, (size_t)c->nb * Nt * H * e));
@@ -364,7 +362,7 @@ dit_status alloc_workspace(dit_cache* c) {
     std::vector<float> one(H, 1.f);
     HIPCK(hipMemcpy(c->ones, one.data(), H * 4, hipMemcpyHostToDevice));
   }
-  c->max_partials = (N + 3) / 4 + 1;
+  c->max_partials = dit::indicator_partials(N);
   TRY(dalloc(c, &c->partials, (size_t)c->max_partials * 4 * sizeof(double)));
   HIPCK(hipHostMalloc((void**)&c->sums_host, 4 * sizeof(double), hipHostMallocMapped));
   HIPCK(hipHostGetDevicePointer((void**)&c->sums_dev, c->sums_host, 0));
@@ -573,19 +571,37 @@ dit_status full_stack(dit_cache* c, int b, const StepCtx& s) {
   return DIT_OK;
 }
 
-// v_b = Final(h_out)
-dit_status final_layer(dit_cache* c, int b, const void* hout, const StepCtx& s, int cls) {
+// v_b = Final(h_out) from the already modulated final-layer input c->yf.
+// Single-branch bf16 sampling folds the Euler update into the projection
+// (x += dsigma v); returns whether it did.
+bool proj_fits(const dit_cache* c) {
+  return c->bf16 && c->C % 16 == 0 && c->C <= 128 && c->H % 32 == 0;
+}
+
+dit_status final_project(dit_cache* c, int b, int cls, float* latent = nullptr, float dsig = 0.f) {
   const int H = c->H, N = c->N;
-  const float* mf = s.modp[b] + (c->n_mod - 2 * H);
-  TRY(ln_mod(c, hout, H, c->yf, H, N, N, mf, mf + H, mf, mf + H, cls));
-  GemmArgs g = lin_args(c, c->yf, H, c->M.fin, c->vel + (size_t)b * N * c->C, c->C, N, DIT_EPI_F32);
   Scope sc(c, cls, 0);
+  if (proj_fits(c)) {
+    HIPCK(dit::launch_proj_small_n(c->yf, H, c->M.fin.w, H, c->M.fin.b, c->vel + (size_t)b * N * c->C, c->C,
+                                   latent, c->C, dsig, N, c->C, H, c->stream));
+    return DIT_OK;
+  }
+  GemmArgs g = lin_args(c, c->yf, H, c->M.fin, c->vel + (size_t)b * N * c->C, c->C, N, DIT_EPI_F32);
   if (c->bf16) {
     HIPCK(dit::launch_gemm_bf16(&g, 1, c->stream, c->n_cu));
   } else {
     HIPCK(dit::launch_gemm_f32(&g, 1, c->stream));
   }
   return DIT_OK;
+}
+
+// full step: y = S(LN(h_out)(1+scale_f)+shift_f), then the projection
+dit_status final_layer(dit_cache* c, int b, const void* hout, const StepCtx& s, int cls, float* latent = nullptr,
+                       float dsig = 0.f) {
+  const int H = c->H, N = c->N;
+  const float* mf = s.modp[b] + (c->n_mod - 2 * H);
+  TRY(ln_mod(c, hout, H, c->yf, H, N, N, mf, mf + H, mf, mf + H, cls));
+  return final_project(c, b, cls, latent, dsig);
 }
 
 // once per sample: text tokens, vec and the modulation table of every step
@@ -695,7 +711,6 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
         sc0 = sh0 + H;
       }
     }
-    int npart = 0;
     {
       Scope sc(c, DIT_K_INDICATOR, (double)N * H * c->esz * (t == 0 ? 2 : (i_prev == i_last ? 3 : 4)));
       TRY(typed(c, [&](auto* tp) {
@@ -710,9 +725,8 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
         return dit::launch_indicator<Ty>((const Ty*)c->h, (Ty*)c->mbuf[i_new],
                                          t ? (const Ty*)c->mbuf[i_prev] : nullptr,
                                          t ? (const Ty*)c->mbuf[i_last] : nullptr, N, H, sh0, sc0,
-                                         t ? c->partials : nullptr, &npart, c->stream);
+                                         t ? c->partials : nullptr, c->sums_dev, c->stream);
       }));
-      if (t) HIPCK(dit::launch_reduce_partials(c->partials, npart, c->sums_dev, c->stream));
     }
 
     // (a3) gate + pacing on the host
@@ -760,26 +774,30 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
       for (int k = 0; k < 4; ++k) out->sums[(size_t)t * 4 + k] = sums[k];
 
     // (a4) full or reuse, (a5) final layer + Euler
+    const float dsig = (float)(sig[t + 1] - sig[t]);
+    const bool fused_euler = !pair && proj_fits(c);
+    float* lat_f = fused_euler ? latent : nullptr;
     for (int b = 0; b < c->nb; ++b) {
       if (dec) {
         TRY(full_stack(c, b, s));
         const void* hout = c->cfg.n_cross ? c->X : sp(c, c->X, (size_t)c->Nt * H);
-        TRY(final_layer(c, b, hout, s, DIT_K_FULL_OTHER));
+        TRY(final_layer(c, b, hout, s, DIT_K_FULL_OTHER, lat_f, dsig));
       } else {
         {
+          // h_out = S(h + r) and the final adaLN in one pass over the rows
           Scope sc(c, DIT_K_REUSE, 3.0 * N * H * c->esz);
+          const float* mf = s.modp[b] + (c->n_mod - 2 * H);
           TRY(typed(c, [&](auto* tp) {
             using Ty = std::remove_pointer_t<decltype(tp)>;
-            return dit::launch_add<Ty>((const Ty*)c->h, (const Ty*)sp(c, c->r, (size_t)b * N * H),
-                                       (Ty*)c->hout, (int64_t)N * H, 1.f, c->stream);
+            return dit::launch_add_ln_mod<Ty>((const Ty*)c->h, (const Ty*)sp(c, c->r, (size_t)b * N * H),
+                                              (Ty*)c->yf, N, H, mf, mf + H, c->stream);
           }));
         }
-        TRY(final_layer(c, b, c->hout, s, DIT_K_REUSE));
+        TRY(final_project(c, b, DIT_K_REUSE, lat_f, dsig));
       }
     }
-    {
+    if (!fused_euler) {
       Scope sc(c, dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
-      const float dsig = (float)(sig[t + 1] - sig[t]);
       HIPCK(dit::launch_euler(latent, c->vel, pair ? c->vel + (size_t)N * c->C : nullptr,
                               (float)p.guidance, dsig, (int64_t)N * c->C, c->stream));
     }
@@ -899,7 +917,7 @@ void dit_cache_destroy(dit_cache* c) {
   if (c->stream) hipStreamSynchronize(c->stream);
   free_per_sample(c);
   void* ps[] = {c->wdev, c->xs, c->h, c->mbuf[0], c->mbuf[1], c->mbuf[2], c->r, c->X, c->A, c->Y, c->vt,
-                c->hout, c->yf, c->vel, c->txt, c->ctxkv, c->vt2, c->ones, c->partials};
+                c->yf, c->vel, c->txt, c->ctxkv, c->vt2, c->ones, c->partials};
   for (void* p : ps)
     if (p) hipFree(p);
   if (c->sums_host) hipHostFree(c->sums_host);

@@ -489,6 +489,57 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
   }
 }
 
+typedef __bf16 bf16x8v_t __attribute__((ext_vector_type(8)));
+
+// Small-N projection (the final layer, N = C <= 128): v[m][c] = sum_k A[m][k] W[c][k]
+// + bias[c], or with x != nullptr the Euler update x[m][c] += alpha * v[m][c]
+// fused in.  16 rows per workgroup, the K range split over 4 waves, MFMA
+// 16x16x32 bf16; A rows stream from HBM once, W (N x K, a few hundred KB)
+// stays in L2.  The 4 partial tiles are summed through LDS in wave order.
+template <int NT>  // N / 16 output tiles
+__global__ __launch_bounds__(256) void proj_small_n_kernel(const bf16_t* __restrict__ A, int64_t lda,
+                                                           const bf16_t* __restrict__ W, int64_t ldw,
+                                                           const bf16_t* __restrict__ bias, float* out,
+                                                           int64_t ldo, float* x, int64_t ldx, float alpha,
+                                                           int M, int K) {
+  __shared__ float part[4][16][NT * 16 + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m0 = blockIdx.x * 16;
+  const int lr = lane & 15, lq = lane >> 4;  // row / column within 16, k-quarter of the 32-deep step
+  const int row = min(m0 + lr, M - 1);
+  const int ksteps = K / 32, per = (ksteps + 3) / 4;
+  const int s0 = wave * per, s1 = min(ksteps, s0 + per);
+  f32x4_t acc[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const bf16_t* ap = A + (int64_t)row * lda + 8 * lq;
+  const bf16_t* wp = W + (int64_t)lr * ldw + 8 * lq;
+#pragma unroll 4
+  for (int st = s0; st < s1; ++st) {
+    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const uint4*)(ap + 32 * st));
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      const bf16x8_t w = __builtin_bit_cast(bf16x8_t, *(const uint4*)(wp + (int64_t)16 * j * ldw + 32 * st));
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w, acc[j], 0, 0, 0);
+    }
+  }
+  // acc[j][i] = C[row 4 lq + i][col 16 j + lr]
+#pragma unroll
+  for (int j = 0; j < NT; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[wave][4 * lq + i][16 * j + lr] = acc[j][i];
+  __syncthreads();
+  for (int e = threadIdx.x; e < 16 * NT * 16; e += 256) {
+    const int r = e / (NT * 16), c = e % (NT * 16);
+    const int m = m0 + r;
+    if (m >= M) continue;
+    float v = part[0][r][c] + part[1][r][c] + part[2][r][c] + part[3][r][c];
+    if (bias) v += bf16_to_f32(bias[c]);
+    if (x) x[(int64_t)m * ldx + c] += alpha * v;
+    else out[(int64_t)m * ldo + c] = v;
+  }
+}
+
 struct Cfg {
   int bm, bn, wn, wg_per_cu, threads, bk;
   bool lds_epi;
@@ -563,6 +614,11 @@ int pick_cfg(const GemmArgs* g, int n, int n_cu) {
   };
   const int f = forced_cfg();
   if (f >= 0 && f < kNumCfgs && admits(kCfgs[f])) return f;
+  bool shallow = true;  // K <= 256: the tile writes dominate, more workgroups stream better
+  for (int i = 0; i < n; ++i) shallow &= g[i].K <= 256 && g[i].M >= 512;
+  if (shallow)
+    for (int c = 0; c < kNumCfgs; ++c)
+      if (kCfgs[c].bm == 128 && kCfgs[c].bn == 128 && admits(kCfgs[c])) return c;
   int best = -1;
   double best_t = 1e300;
   for (int c = 0; c < kNumCfgs; ++c) {
@@ -580,6 +636,25 @@ int pick_cfg(const GemmArgs* g, int n, int n_cu) {
 }
 
 }  // namespace
+
+hipError_t launch_proj_small_n(const void* A, int64_t lda, const void* W, int64_t ldw, const void* bias,
+                               float* out, int64_t ldo, float* x, int64_t ldx, float alpha, int M, int N,
+                               int K, hipStream_t s) {
+  if (K % 32 || N % 16 || N > 128 || M < 1) return hipErrorInvalidValue;
+  const dim3 grid((M + 15) / 16);
+#define DIT_PROJ(NT_)                                                                             \
+  case NT_:                                                                                       \
+    hipLaunchKernelGGL(proj_small_n_kernel<NT_>, grid, dim3(256), 0, s, (const bf16_t*)A, lda,     \
+                       (const bf16_t*)W, ldw, (const bf16_t*)bias, out, ldo, x, ldx, alpha, M, K); \
+    break;
+  switch (N / 16) {
+    DIT_PROJ(1) DIT_PROJ(2) DIT_PROJ(3) DIT_PROJ(4) DIT_PROJ(5) DIT_PROJ(6) DIT_PROJ(7) DIT_PROJ(8)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef DIT_PROJ
+  return hipGetLastError();
+}
 
 hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t stream, int n_cu) {
   if (n < 1 || n > 2) return hipErrorInvalidValue;

@@ -24,6 +24,11 @@ struct GemmArgs {
 
 // bf16 MFMA GEMM; n = 1 or 2 independent problems in one launch.
 hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t s, int n_cu);
+// v = A W^T + bias for N <= 128 (multiple of 16), K % 32 == 0, f32 output; with
+// x != nullptr the result goes into the Euler update x += alpha * v instead.
+hipError_t launch_proj_small_n(const void* A, int64_t lda, const void* W, int64_t ldw, const void* bias,
+                               float* out, int64_t ldo, float* x, int64_t ldx, float alpha, int M, int N,
+                               int K, hipStream_t s);
 // f32 GEMM (small f32 workloads); bias f32; rms_cols handled by rms_heads_f32.
 hipError_t launch_gemm_f32(const GemmArgs* g, int n, hipStream_t s);
 
@@ -47,13 +52,18 @@ hipError_t launch_ln_mod(const T* x, int64_t ldx, T* out, int64_t ldo, int rows,
                          const float* sh0, const float* sc0, const float* sh1, const float* sc1,
                          hipStream_t s);
 // Indicator: m = S(LN(h)(1+sc)+sh) (or m = h when sc == nullptr), written
-// to m_out; per-block partial sums (f64) of |m-mp|, |mp|, |m-ml|, |ml|.
+// to m_out; with partials != nullptr the relative-L1 sums |m-mp|, |mp|,
+// |m-ml|, |ml| are reduced in a fixed order into out[4] (f64, host-mapped)
+// through `partials` (indicator_partials(rows) 4-vectors).
 template <typename T>
 hipError_t launch_indicator(const T* h, T* m_out, const T* m_prev, const T* m_last, int rows,
-                            int H, const float* sh, const float* sc, double* partials,
-                            int* n_partials, hipStream_t s);
-// Fixed-order f64 reduction of n partial 4-vectors into out[4] (host-mapped).
-hipError_t launch_reduce_partials(const double* partials, int n, double* out, hipStream_t s);
+                            int H, const float* sh, const float* sc, double* partials, double* out,
+                            hipStream_t s);
+int indicator_partials(int rows);
+// y = S(LN(S(a + b))(1+sc)+sh) per row (reuse-step final-layer input).
+template <typename T>
+hipError_t launch_add_ln_mod(const T* a, const T* b, T* out, int rows, int H, const float* sh,
+                             const float* sc, hipStream_t s);
 // r = S(a - b) (refresh) or r = S(a + b) (reuse), n elements.
 template <typename T>
 hipError_t launch_add(const T* a, const T* b, T* out, int64_t n, float sign, hipStream_t s);

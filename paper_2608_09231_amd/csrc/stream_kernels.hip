@@ -25,6 +25,14 @@ template <> struct Chunk<bf16_t> {
       v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
     }
   }
+  static __device__ __forceinline__ void unpack(const uint4& u, float (&v)[8]) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
   static __device__ __forceinline__ void store(bf16_t* p, const float (&v)[8]) {
     *(uint4*)p = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                             pack_bf16x2(v[6], v[7]));
@@ -35,6 +43,10 @@ template <> struct Chunk<float> {
   static __device__ __forceinline__ void load(const float* p, float (&v)[4]) {
     const float4 u = *(const float4*)p;
     v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+  }
+  static __device__ __forceinline__ void unpack(const uint4& u, float (&v)[4]) {
+    v[0] = __uint_as_float(u.x); v[1] = __uint_as_float(u.y);
+    v[2] = __uint_as_float(u.z); v[3] = __uint_as_float(u.w);
   }
   static __device__ __forceinline__ void store(float* p, const float (&v)[4]) {
     *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
@@ -127,8 +139,10 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, in
 
 // Indicator: each wave handles IRW consecutive rows; m = S(LN(h)(1+sc)+sh)
 // (or m = h when sc == nullptr) is written, and |m - mp|, |mp|, |m - ml|,
-// |ml| are summed per lane, then per workgroup (f64 partial 4-vector).
-constexpr int IRW = 4;
+// |ml| are summed per lane, then per workgroup (f64 partial 4-vector).  The
+// rows of m_prev / m_last are loaded together with h, before the
+// statistics, so the three streams are in flight at once.
+constexpr int IRW = 1;
 constexpr int IROWS = 4 * IRW;  // rows per workgroup
 
 template <typename T, int MAXC>
@@ -148,6 +162,17 @@ __global__ __launch_bounds__(256) void indicator_kernel(const T* __restrict__ h,
     const int64_t base = (int64_t)row * H;
     RowRegs<T, MAXC> r;
     r.load(h + base, H, lane);
+    uint4 pv[MAXC], lv[MAXC];
+    if (mp) {
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) {
+        const int c = lane + 64 * j;
+        if (c < r.nch) {
+          pv[j] = *(const uint4*)(mp + base + c * E);
+          if (!same) lv[j] = *(const uint4*)(ml + base + c * E);
+        }
+      }
+    }
     float mean = 0.f, rstd = 1.f;
     if (sc) r.stats(H, lane, mean, rstd);
 #pragma unroll
@@ -167,14 +192,13 @@ __global__ __launch_bounds__(256) void indicator_kernel(const T* __restrict__ h,
       }
       Chunk<T>::store(m + base + c * E, y);
       if (mp) {
-        float p[E];
-        Chunk<T>::load(mp + base + c * E, p);
-        float l[E];
+        float p[E], l[E];
+        Chunk<T>::unpack(pv[j], p);
         if (same) {
 #pragma unroll
           for (int e = 0; e < E; ++e) l[e] = p[e];
         } else {
-          Chunk<T>::load(ml + base + c * E, l);
+          Chunk<T>::unpack(lv[j], l);
         }
 #pragma unroll
         for (int e = 0; e < E; ++e) {
@@ -199,7 +223,8 @@ __global__ __launch_bounds__(256) void indicator_kernel(const T* __restrict__ h,
 }
 
 // Fixed-order f64 sum of n partial 4-vectors: thread t sums t, t+256, ...,
-// then a fixed binary tree.  Deterministic for a given n.
+// then a fixed binary tree.  Deterministic for a given n.  `out` is
+// host-mapped pinned memory.
 __global__ __launch_bounds__(256) void reduce_partials_kernel(const double* __restrict__ p, int n,
                                                               double* out) {
   __shared__ double s[4][256];
@@ -220,12 +245,60 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(const double* __re
   __threadfence_system();
 }
 
+// Reuse-step final-layer input: y = S(LN(S(a + b)) (1 + sc) + sh), one wave
+// per row (a = h, b = cached residual r).
+template <typename T, int MAXC>
+__global__ __launch_bounds__(256) void add_ln_mod_kernel(const T* __restrict__ a, const T* __restrict__ b,
+                                                        T* __restrict__ out, int rows, int H,
+                                                        const float* sh, const float* sc) {
+  constexpr int E = Chunk<T>::E;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int64_t base = (int64_t)row * H;
+  RowRegs<T, MAXC> r;
+  r.load(a + base, H, lane);
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    const int c = lane + 64 * j;
+    if (c < r.nch) {
+      float q[E];
+      Chunk<T>::load(b + base + c * E, q);
+#pragma unroll
+      for (int e = 0; e < E; ++e) r.v[j][e] = St<T>::rd(r.v[j][e] + q[e]);
+    }
+  }
+  float mean, rstd;
+  r.stats(H, lane, mean, rstd);
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    const int c = lane + 64 * j;
+    if (c < r.nch) {
+      float y[E], s1[E], s2[E];
+      load_mod(sc + c * E, s1);
+      load_mod(sh + c * E, s2);
+#pragma unroll
+      for (int e = 0; e < E; ++e) y[e] = (r.v[j][e] - mean) * rstd * (1.f + s1[e]) + s2[e];
+      Chunk<T>::store(out + base + c * E, y);
+    }
+  }
+}
+
+// out = S(a + sign b), 16-byte vectors (n is a multiple of the vector width).
 template <typename T>
 __global__ void add_kernel(const T* __restrict__ a, const T* __restrict__ b, T* __restrict__ out,
                            int64_t n, float sign) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * blockDim.x)
-    St<T>::st(out + i, St<T>::ld(a + i) + sign * St<T>::ld(b + i));
+  constexpr int E = Chunk<T>::E;
+  const int64_t nv = n / E;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    float x[E], y[E];
+    Chunk<T>::load(a + i * E, x);
+    Chunk<T>::load(b + i * E, y);
+#pragma unroll
+    for (int e = 0; e < E; ++e) x[e] += sign * y[e];
+    Chunk<T>::store(out + i * E, x);
+  }
 }
 
 __global__ void euler_kernel(float* __restrict__ x, const float* __restrict__ vc,
@@ -336,26 +409,37 @@ hipError_t launch_ln_mod(const T* x, int64_t ldx, T* out, int64_t ldo, int rows,
 
 template <typename T>
 hipError_t launch_indicator(const T* h, T* m_out, const T* m_prev, const T* m_last, int rows, int H,
-                            const float* sh, const float* sc, double* partials, int* n_partials,
-                            hipStream_t s) {
+                            const float* sh, const float* sc, double* partials, double* out, hipStream_t s) {
   if (H % Chunk<T>::E) return hipErrorInvalidValue;
   const int nb = (rows + IROWS - 1) / IROWS;
-  if (n_partials) *n_partials = nb;
-  return dispatch_maxc<T>(H, [&](auto mc) {
+  hipError_t e = dispatch_maxc<T>(H, [&](auto mc) {
     hipLaunchKernelGGL((indicator_kernel<T, decltype(mc)::value>), dim3(nb), dim3(256), 0, s, h, m_out,
                        m_prev, m_last, rows, H, sh, sc, partials);
     return hipGetLastError();
   });
-}
-
-hipError_t launch_reduce_partials(const double* partials, int n, double* out, hipStream_t s) {
-  hipLaunchKernelGGL(reduce_partials_kernel, dim3(1), dim3(256), 0, s, partials, n, out);
+  if (e != hipSuccess || !partials) return e;
+  hipLaunchKernelGGL(reduce_partials_kernel, dim3(1), dim3(256), 0, s, partials, nb, out);
   return hipGetLastError();
 }
 
 template <typename T>
+hipError_t launch_add_ln_mod(const T* a, const T* b, T* out, int rows, int H, const float* sh,
+                             const float* sc, hipStream_t s) {
+  if (H % Chunk<T>::E) return hipErrorInvalidValue;
+  if (rows <= 0) return hipSuccess;
+  return dispatch_maxc<T>(H, [&](auto mc) {
+    hipLaunchKernelGGL((add_ln_mod_kernel<T, decltype(mc)::value>), dim3((rows + 3) / 4), dim3(256), 0, s,
+                       a, b, out, rows, H, sh, sc);
+    return hipGetLastError();
+  });
+}
+
+int indicator_partials(int rows) { return (rows + IROWS - 1) / IROWS; }
+
+template <typename T>
 hipError_t launch_add(const T* a, const T* b, T* out, int64_t n, float sign, hipStream_t s) {
-  hipLaunchKernelGGL(add_kernel<T>, dim3(grid_for(n, 256)), dim3(256), 0, s, a, b, out, n, sign);
+  if (n % Chunk<T>::E) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(add_kernel<T>, dim3(grid_for(n / Chunk<T>::E, 256)), dim3(256), 0, s, a, b, out, n, sign);
   return hipGetLastError();
 }
 
@@ -413,7 +497,9 @@ hipError_t launch_add_offset(const float* mod, int64_t ld, int base, const T* of
   template hipError_t launch_ln_mod<T>(const T*, int64_t, T*, int64_t, int, int, int, const float*, \
                                        const float*, const float*, const float*, hipStream_t);     \
   template hipError_t launch_indicator<T>(const T*, T*, const T*, const T*, int, int, const float*, \
-                                          const float*, double*, int*, hipStream_t);               \
+                                          const float*, double*, double*, hipStream_t);            \
+  template hipError_t launch_add_ln_mod<T>(const T*, const T*, T*, int, int, const float*, const float*, \
+                                           hipStream_t);                                           \
   template hipError_t launch_add<T>(const T*, const T*, T*, int64_t, float, hipStream_t);         \
   template hipError_t launch_cast_from_f32<T>(const float*, T*, int64_t, hipStream_t);            \
   template hipError_t launch_time_embed<T>(const double*, T*, int, int, hipStream_t);             \
