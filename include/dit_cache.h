@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define DIT_ABI_VERSION 1
+#define DIT_ABI_VERSION 2
 #define DIT_N_FEATURES 8
 
 typedef enum dit_status {
@@ -102,6 +102,20 @@ typedef struct dit_model_config {
  * (shift, scale). */
 
 /* Per-call sampler parameters. */
+/* Decision policies (Sec. 3 states the three paradigms on one cost model:
+ * every policy runs the same kernels and records the same features).
+ *   GATE       Alg. 2: the gate's vote z_t > ln(tau/(1-tau)), overridden by
+ *              the budget rules; realised NFE = B.
+ *   STATIC     m = mu(B, T), fixed before sampling: computed steps at
+ *              t_i = floor(i T / B), i = 0..B-1; realised NFE = B.  The
+ *              gate blob is not read (may be NULL).
+ *   THRESHOLD  online rule m_t = [q_t > delta], q_t = relative-L1 change of
+ *              the indicator accumulated since the last computed step
+ *              (feature f7); t = 0 computes; no budget rule, so the realised
+ *              NFE is whatever the rule spends (B enters only the features).
+ *              The gate blob is not read (may be NULL). */
+enum { DIT_POLICY_GATE = 0, DIT_POLICY_STATIC = 1, DIT_POLICY_THRESHOLD = 2 };
+
 typedef struct dit_sample_params {
   int32_t T;                    /* steps, >= 1 */
   int32_t B;                    /* full evaluations, 1 <= B <= T */
@@ -109,19 +123,22 @@ typedef struct dit_sample_params {
   double shift;                 /* used when sigmas == NULL: sigma_i = s u / (1 + (s-1) u), u = 1 - i/T */
   double tau;                   /* cutoff on sigma(z), in (0, 1); the paper uses 0.5 */
   double guidance;              /* guidance scale g, used when batch == 2 */
-  const uint8_t* forced_mask;   /* host [T] replay mask (m_0 = 1, exactly B ones) or NULL */
+  const uint8_t* forced_mask;   /* host [T] replay mask (m_0 = 1; exactly B ones unless the
+                                   policy is DIT_POLICY_THRESHOLD) or NULL */
   int32_t indicator;            /* DIT_INDICATOR_MODULATED (default) or DIT_INDICATOR_PATCH */
+  int32_t policy;               /* DIT_POLICY_GATE (default), _STATIC or _THRESHOLD */
+  double delta;                 /* DIT_POLICY_THRESHOLD's cutoff on q_t */
 } dit_sample_params;
 
 /* Per-step record, host arrays owned by the caller (each may be NULL
  * except `full`). */
 typedef struct dit_schedule {
   uint8_t* full;       /* [T] 1 = network evaluated and cache refreshed, 0 = residual reused */
-  float* logit;        /* [T] gate logit z_t (NaN at t = 0, where no gate runs) */
+  float* logit;        /* [T] gate logit z_t (THRESHOLD: q_t; NaN at t = 0 and under STATIC) */
   uint8_t* forced;     /* [T] 1 where a budget rule (or t = 0) fixed the decision */
   double* features;    /* [T * 8] gate inputs f0..f7 (NaN row at t = 0) */
   double* sums;        /* [T * 4] sum|m_t-m_{t-1}|, sum|m_{t-1}|, sum|m_t-m_last|, sum|m_last| */
-  int32_t nfe;         /* out: computed steps (== B on success) */
+  int32_t nfe;         /* out: computed steps (== B on success unless THRESHOLD) */
   int32_t steps_done;  /* out: steps completed */
 } dit_schedule;
 

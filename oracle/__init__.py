@@ -22,8 +22,8 @@ checked against this oracle only).
 """
 from .numerics import round_bf16, round_f32, round_storage
 from .gate import Gate, parse_gate_blob
-from .sampler import sample, sigma_schedule, SampleResult, decide, budget_features
+from .sampler import sample, sigma_schedule, static_schedule, SampleResult, decide, budget_features
 from . import dit
 
 __all__ = ["round_bf16", "round_f32", "round_storage", "Gate", "parse_gate_blob",
-           "sample", "sigma_schedule", "SampleResult", "decide", "budget_features", "dit"]
+           "sample", "sigma_schedule", "static_schedule", "SampleResult", "decide", "budget_features", "dit"]

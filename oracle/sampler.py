@@ -24,6 +24,16 @@ exactly Eq. 3's s_bud and s_traj):
   f4 = |m_t - m_last|_1 / |m_last|_1, f5 = |m_t - m_{t-1}|_1 / |m_{t-1}|_1,
   f6 = t/T (step fraction), f7 = sum of f5 since the last computed step.
 c = computed steps before t; denominators are max(sum, 1e-30).
+
+Decision policies (Sec. 3, the paradigms BAG is compared with, run on the
+same steps and the same state):
+  "gate"      Alg. 2: the learned gate plus the two budget rules.
+  "static"    m = mu(B, T), fixed before sampling from B and T alone: the
+              B computed steps spread uniformly, t_i = floor(i T / B).
+  "threshold" online rule m_t = [q_t > delta] with q_t = f7, the relative
+              L1 change of the indicator accumulated since the last
+              computed step; no budget rule, so the realised NFE is
+              whatever the rule spends (B only enters the features).
 """
 from dataclasses import dataclass, field
 
@@ -63,6 +73,13 @@ def decide(z, B, T, t, c, tau=0.5):
     return m, forced
 
 
+def static_schedule(B, T):
+    """mu(B, T): ones at t_i = floor(i T / B), i = 0..B-1 (m_0 = 1, B ones)."""
+    m = np.zeros(T, np.uint8)
+    m[[(i * T) // B for i in range(B)]] = 1
+    return m
+
+
 def rel_l1_sums(a, b):
     """(sum |a - b|, sum |b|) in float64."""
     return float(np.abs(a - b).sum()), float(np.abs(b).sum())
@@ -82,7 +99,7 @@ class SampleResult:
 
 def sample(cfg, weights, gate_blob, x0, text, T, B, *, sigmas=None, shift=1.0,
            tau=0.5, guidance=1.0, forced_mask=None, indicator="modulated",
-           trace=False, gate_fn=None):
+           trace=False, gate_fn=None, policy="gate", delta=0.0):
     """Run one cached sample.
 
     cfg       model config (attributes as in the workload registry)
@@ -91,21 +108,29 @@ def sample(cfg, weights, gate_blob, x0, text, T, B, *, sigmas=None, shift=1.0,
     x0        float32 [N, C]; text: storage [batch, N_t, ctx]
     forced_mask optional uint8 [T]: replaces every decision (replay)
     gate_fn   optional callable(features) -> logit, for tests
+    policy    "gate" | "static" | "threshold" (module docstring); delta is
+              the threshold rule's cutoff
     """
     if not (1 <= B <= T):
         raise ValueError("budget must satisfy 1 <= B <= T")
+    if policy not in ("gate", "static", "threshold"):
+        raise ValueError("unknown policy")
+    mu = static_schedule(B, T) if policy == "static" else None
     P = dit.Params(cfg, weights)
     rs = P.rs
-    gate = None if gate_fn is not None else parse_gate_blob(gate_blob)
-    logit_fn = gate_fn if gate_fn is not None else gate.logit
+    logit_fn = None
+    if policy == "gate":
+        logit_fn = gate_fn if gate_fn is not None else parse_gate_blob(gate_blob).logit
     if sigmas is None:
         sigmas = sigma_schedule(T, shift)
     sigmas = np.asarray(sigmas, np.float64)
     assert sigmas.shape == (T + 1,)
     if forced_mask is not None:
         forced_mask = np.asarray(forced_mask, np.uint8)
-        if forced_mask.shape != (T,) or forced_mask[0] != 1 or int(forced_mask.sum()) != B:
-            raise ValueError("forced mask must have m_0 = 1 and exactly B ones")
+        if forced_mask.shape != (T,) or forced_mask[0] != 1:
+            raise ValueError("forced mask must have m_0 = 1")
+        if policy != "threshold" and int(forced_mask.sum()) != B:
+            raise ValueError("forced mask must have exactly B ones")
 
     nb = cfg.batch
     text64 = [storage_to_f64(text[b], cfg.dtype) for b in range(nb)]
@@ -143,9 +168,15 @@ def sample(cfg, weights, gate_blob, x0, text, T, B, *, sigmas=None, shift=1.0,
             acc += d_prev
             f = budget_features(B, T, t, c) + [float(t - t_last), d_last, d_prev, t / T, acc]
             feats[t] = f
-            z = logit_fn(np.asarray(f))
-            logit[t] = z
-            dec, frc = decide(z, B, T, t, c, tau)
+            if policy == "gate":
+                z = logit_fn(np.asarray(f))
+                logit[t] = z
+                dec, frc = decide(z, B, T, t, c, tau)
+            elif policy == "static":
+                dec, frc = int(mu[t]), 0
+            else:
+                logit[t] = acc
+                dec, frc = (1 if acc > delta else 0), 0
             if forced_mask is not None:
                 dec = int(forced_mask[t])
         full[t], forced[t] = dec, frc
@@ -175,7 +206,7 @@ def sample(cfg, weights, gate_blob, x0, text, T, B, *, sigmas=None, shift=1.0,
             tr["r"].append([None if rb is None else rb.copy() for rb in r])
             tr["v"].append(v)
 
-    if c != B:
+    if c != B and policy != "threshold":
         raise AssertionError(f"realised NFE {c} != budget {B}")
     return SampleResult(x=x, full=full, logit=logit, forced=forced, features=feats,
                         sums=sums, nfe=c, trace=tr)

@@ -22,7 +22,8 @@ STATUS_NAMES = {0: "DIT_OK", -1: "DIT_EINVAL", -2: "DIT_ENOMEM", -3: "DIT_EHIP",
 DTYPE_F32, DTYPE_BF16 = 0, 1
 INDICATOR_MODULATED, INDICATOR_PATCH = 0, 1
 EPI_STORE, EPI_F32, EPI_GATED_RES, EPI_SILU = 0, 1, 2, 4
-ABI_VERSION = 1
+ABI_VERSION = 2
+POLICIES = {"gate": 0, "static": 1, "threshold": 2}
 N_FEATURES = 8
 K_CLASSES = ["gemm", "attn", "indicator", "reuse", "full_other", "once"]
 
@@ -41,7 +42,8 @@ class ModelConfigC(C.Structure):
 class SampleParamsC(C.Structure):
     _fields_ = [("T", C.c_int32), ("B", C.c_int32), ("sigmas", C.POINTER(C.c_double)),
                 ("shift", C.c_double), ("tau", C.c_double), ("guidance", C.c_double),
-                ("forced_mask", C.POINTER(C.c_uint8)), ("indicator", C.c_int32)]
+                ("forced_mask", C.POINTER(C.c_uint8)), ("indicator", C.c_int32),
+                ("policy", C.c_int32), ("delta", C.c_double)]
 
 
 class ScheduleC(C.Structure):
@@ -162,11 +164,13 @@ class DitCache:
             pass
 
     def sample(self, latent, text_emb, gate_blob, T, B, *, sigmas=None, shift=1.0, tau=0.5,
-               guidance=1.0, forced_mask=None, indicator="modulated") -> Schedule:
+               guidance=1.0, forced_mask=None, indicator="modulated", policy="gate",
+               delta=0.0) -> Schedule:
         """latent: torch f32 cuda [N, C] (in place); text_emb: torch cuda
         storage-dtype [batch, N_t, ctx] (bf16 workloads: int16/uint16 bits
-        or torch.bfloat16)."""
-        gate = np.ascontiguousarray(gate_blob, np.float32)
+        or torch.bfloat16); policy "gate" | "static" | "threshold" (the
+        latter two do not read gate_blob, which may be None)."""
+        gate = np.ascontiguousarray(gate_blob if gate_blob is not None else [], np.float32)
         full = np.zeros(T, np.uint8)
         logit = np.zeros(T, np.float32)
         forced = np.zeros(T, np.uint8)
@@ -183,10 +187,12 @@ class DitCache:
                           sig.ctypes.data_as(C.POINTER(C.c_double)) if sig is not None else None,
                           float(shift), float(tau), float(guidance),
                           fm.ctypes.data_as(C.POINTER(C.c_uint8)) if fm is not None else None,
-                          INDICATOR_PATCH if indicator == "patch" else INDICATOR_MODULATED)
+                          INDICATOR_PATCH if indicator == "patch" else INDICATOR_MODULATED,
+                          POLICIES[policy], float(delta))
         st = _lib.dit_cache_sample_ex(self._h, C.c_void_p(latent.data_ptr()),
                                       C.c_void_p(text_emb.data_ptr()),
-                                      gate.ctypes.data_as(C.c_void_p), gate.size, C.byref(p),
+                                      gate.ctypes.data_as(C.c_void_p) if gate.size else None, gate.size,
+                                      C.byref(p),
                                       C.byref(sched))
         res = Schedule(full, logit, forced, feats.reshape(T, N_FEATURES), sums.reshape(T, 4),
                        sched.nfe, sched.steps_done)

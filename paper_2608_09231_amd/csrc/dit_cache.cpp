@@ -44,11 +44,21 @@ struct Model {
   std::vector<CrossW> crs;
 };
 
-struct GateMLP {
+// One dense ReLU network: widths d_0..d_{k-1}, layers W_l [d_l, d_{l-1}].
+struct DenseNet {
   std::vector<int> widths;
+  std::vector<std::vector<double>> W, b;
+};
+
+// The gate: optional branches (each reads the next d_0 features, ReLU after
+// every layer) feeding a trunk (ReLU after every hidden layer, none on the
+// logit); without branches the trunk reads the features directly.
+struct GateMLP {
+  int d_in = 0;
   bool z = false;
   std::vector<double> mu, sd;
-  std::vector<std::vector<double>> W, b;
+  std::vector<DenseNet> branches;
+  DenseNet trunk;
 };
 
 struct Pending {
@@ -400,53 +410,110 @@ dit_status ensure_T(dit_cache* c, int T) {
 }
 
 // ---------------------------------------------------------------- gate
+// Reads "k, d_0..d_{k-1}" at blob[p]; false on a malformed header.
+bool read_widths(const float* blob, size_t n, size_t& p, std::vector<int>& w) {
+  if (p >= n) return false;
+  const double k = blob[p];
+  if (k < 2 || k > 16 || k != std::floor(k) || p + 1 + (size_t)k > n) return false;
+  w.resize((int)k);
+  for (int i = 0; i < (int)k; ++i) {
+    const double v = blob[p + 1 + i];
+    if (v < 1 || v > 4096 || v != std::floor(v)) return false;
+    w[i] = (int)v;
+  }
+  p += 1 + (size_t)k;
+  return true;
+}
+
+size_t net_params(const DenseNet& d) {
+  size_t m = 0;
+  for (size_t i = 1; i < d.widths.size(); ++i) m += (size_t)d.widths[i] * d.widths[i - 1] + d.widths[i];
+  return m;
+}
+
+void read_params(const float* blob, size_t& p, DenseNet& d) {
+  d.W.clear(); d.b.clear();
+  for (size_t i = 1; i < d.widths.size(); ++i) {
+    const size_t nw = (size_t)d.widths[i] * d.widths[i - 1];
+    d.W.emplace_back(blob + p, blob + p + nw); p += nw;
+    d.b.emplace_back(blob + p, blob + p + d.widths[i]); p += d.widths[i];
+  }
+}
+
+// Eq. 1's gate from its self-describing blob: a plain MLP
+// [k, widths, zflag, (mu, sd), params] or a branched network
+// [-n, (k_j, widths_j) x n, k, trunk widths, zflag, (mu, sd), params of
+// branch 1..n, params of the trunk] (App. A.2's two-group gate).
 dit_status parse_gate(dit_cache* c, const float* blob, size_t n, GateMLP& g) {
   if (!blob || n < 4) return fail(c, DIT_EINVAL, "gate blob missing or too short");
-  const double k = blob[0];
-  if (k < 2 || k > 16 || k != std::floor(k)) return fail(c, DIT_EINVAL, "gate blob: bad layer count");
-  const int kk = (int)k;
-  if (n < (size_t)(2 + kk)) return fail(c, DIT_EINVAL, "gate blob too short");
-  g.widths.resize(kk);
-  for (int i = 0; i < kk; ++i) {
-    const double w = blob[1 + i];
-    if (w < 1 || w > 4096 || w != std::floor(w)) return fail(c, DIT_EINVAL, "gate blob: bad width");
-    g.widths[i] = (int)w;
+  size_t p = 0;
+  g.branches.clear();
+  if (blob[0] < 0) {
+    const double nb = -(double)blob[0];
+    if (nb != std::floor(nb) || nb > DIT_N_FEATURES) return fail(c, DIT_EINVAL, "gate blob: bad branch count");
+    p = 1;
+    g.branches.resize((int)nb);
+    for (auto& br : g.branches)
+      if (!read_widths(blob, n, p, br.widths)) return fail(c, DIT_EINVAL, "gate blob: bad branch header");
   }
-  if (g.widths.back() != 1) return fail(c, DIT_EINVAL, "gate blob: output width must be 1");
-  if (g.widths[0] > DIT_N_FEATURES) return fail(c, DIT_EINVAL, "gate blob: more than 8 inputs");
-  size_t p = 1 + kk;
+  if (!read_widths(blob, n, p, g.trunk.widths)) return fail(c, DIT_EINVAL, "gate blob: bad layer count");
+  if (g.trunk.widths.back() != 1) return fail(c, DIT_EINVAL, "gate blob: output width must be 1");
+  int d_in = g.trunk.widths[0];
+  if (!g.branches.empty()) {
+    int outs = 0;
+    d_in = 0;
+    for (auto& br : g.branches) { outs += br.widths.back(); d_in += br.widths[0]; }
+    if (outs != g.trunk.widths[0])
+      return fail(c, DIT_EINVAL, "gate blob: trunk input width != sum of branch outputs");
+  }
+  if (d_in > DIT_N_FEATURES) return fail(c, DIT_EINVAL, "gate blob: more than 8 inputs");
+  g.d_in = d_in;
+  if (p >= n) return fail(c, DIT_EINVAL, "gate blob: length mismatch");
   g.z = blob[p++] != 0.f;
-  size_t need = p + (g.z ? 2 * g.widths[0] : 0);
-  for (int i = 1; i < kk; ++i) need += (size_t)g.widths[i] * g.widths[i - 1] + g.widths[i];
+  size_t need = p + (g.z ? 2 * (size_t)d_in : 0) + net_params(g.trunk);
+  for (auto& br : g.branches) need += net_params(br);
   if (need != n) return fail(c, DIT_EINVAL, "gate blob: length mismatch");
   if (g.z) {
-    g.mu.assign(blob + p, blob + p + g.widths[0]); p += g.widths[0];
-    g.sd.assign(blob + p, blob + p + g.widths[0]); p += g.widths[0];
+    g.mu.assign(blob + p, blob + p + d_in); p += d_in;
+    g.sd.assign(blob + p, blob + p + d_in); p += d_in;
   }
-  g.W.clear(); g.b.clear();
-  for (int i = 1; i < kk; ++i) {
-    const size_t nw = (size_t)g.widths[i] * g.widths[i - 1];
-    g.W.emplace_back(blob + p, blob + p + nw); p += nw;
-    g.b.emplace_back(blob + p, blob + p + g.widths[i]); p += g.widths[i];
-  }
+  for (auto& br : g.branches) read_params(blob, p, br);
+  read_params(blob, p, g.trunk);
   return DIT_OK;
 }
 
-double gate_logit(const GateMLP& g, const double* f) {
-  std::vector<double> u(f, f + g.widths[0]), nx;
-  if (g.z)
-    for (int i = 0; i < g.widths[0]; ++i) u[i] = (u[i] - g.mu[i]) / g.sd[i];
-  const int nl = (int)g.W.size();
+// u <- net(u), in float64; ReLU after every layer but the last unless last_relu.
+void dense_forward(const DenseNet& d, std::vector<double>& u, bool last_relu) {
+  std::vector<double> nx;
+  const int nl = (int)d.W.size();
   for (int l = 0; l < nl; ++l) {
-    const int o = g.widths[l + 1], in = g.widths[l];
+    const int o = d.widths[l + 1], in = d.widths[l];
     nx.assign(o, 0.0);
     for (int j = 0; j < o; ++j) {
-      double s = g.b[l][j];
-      for (int i = 0; i < in; ++i) s += g.W[l][(size_t)j * in + i] * u[i];
-      nx[j] = (l < nl - 1) ? (s > 0.0 ? s : 0.0) : s;
+      double s = d.b[l][j];
+      for (int i = 0; i < in; ++i) s += d.W[l][(size_t)j * in + i] * u[i];
+      nx[j] = (l < nl - 1 || last_relu) ? (s > 0.0 ? s : 0.0) : s;
     }
     u.swap(nx);
   }
+}
+
+double gate_logit(const GateMLP& g, const double* f) {
+  std::vector<double> u(f, f + g.d_in);
+  if (g.z)
+    for (int i = 0; i < g.d_in; ++i) u[i] = (u[i] - g.mu[i]) / g.sd[i];
+  if (!g.branches.empty()) {
+    std::vector<double> cat, part;
+    int off = 0;
+    for (const auto& br : g.branches) {
+      part.assign(u.begin() + off, u.begin() + off + br.widths[0]);
+      off += br.widths[0];
+      dense_forward(br, part, true);
+      cat.insert(cat.end(), part.begin(), part.end());
+    }
+    u.swap(cat);
+  }
+  dense_forward(g.trunk, u, false);
   return u[0];
 }
 
@@ -685,6 +752,9 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
   s.T = T;
   const bool pair = c->nb == 2;
   const double thr = std::log(p.tau / (1.0 - p.tau));
+  // mu(B, T) of the static policy: computed steps at floor(i T / B)
+  std::vector<uint8_t> mu(T, 0);
+  for (int i = 0; i < B; ++i) mu[(size_t)((int64_t)i * T / B)] = 1;
   int cnt = 0, t_last = 0;
   double acc = 0.0;
   int i_prev = -1, i_last = -1;
@@ -756,11 +826,18 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
       f[5] = d_prev;
       f[6] = (double)t / T;
       f[7] = acc;
-      z = gate_logit(gate, f);
-      dec = (z > thr) ? 1 : 0;
       forced = 0;
-      if (B - cnt >= T - t) { dec = 1; forced = 1; }
-      if (B - cnt == 0) { dec = 0; forced = 1; }
+      if (p.policy == DIT_POLICY_GATE) {
+        z = gate_logit(gate, f);
+        dec = (z > thr) ? 1 : 0;
+        if (B - cnt >= T - t) { dec = 1; forced = 1; }
+        if (B - cnt == 0) { dec = 0; forced = 1; }
+      } else if (p.policy == DIT_POLICY_STATIC) {
+        dec = mu[t];
+      } else {
+        z = acc;
+        dec = (acc > p.delta) ? 1 : 0;
+      }
       if (p.forced_mask) dec = p.forced_mask[t] ? 1 : 0;
       c->stats.host_gate_ms +=
           std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - h0).count();
@@ -815,7 +892,8 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
     out->steps_done = t + 1;
   }
   HIPCK(hipStreamSynchronize(c->stream));
-  if (cnt != B) return fail(c, DIT_EBUDGET, "realised NFE differs from the budget");
+  if (cnt != B && p.policy != DIT_POLICY_THRESHOLD)
+    return fail(c, DIT_EBUDGET, "realised NFE differs from the budget");
   return DIT_OK;
 }
 
@@ -885,16 +963,22 @@ dit_status dit_cache_sample_ex(dit_cache* c, float* latent, const void* text_emb
   if (p->indicator != DIT_INDICATOR_MODULATED && p->indicator != DIT_INDICATOR_PATCH)
     return fail(c, DIT_EINVAL, "bad indicator");
   if (!p->sigmas && !(p->shift > 0.0)) return fail(c, DIT_EINVAL, "shift must be > 0");
+  if (p->policy != DIT_POLICY_GATE && p->policy != DIT_POLICY_STATIC && p->policy != DIT_POLICY_THRESHOLD)
+    return fail(c, DIT_EINVAL, "bad policy");
+  if (p->policy == DIT_POLICY_THRESHOLD && std::isnan(p->delta))
+    return fail(c, DIT_EINVAL, "threshold delta is NaN");
   if (p->forced_mask) {
     int ones = 0;
     for (int t = 0; t < p->T; ++t) {
       if (p->forced_mask[t] > 1) return fail(c, DIT_EINVAL, "forced mask entries must be 0/1");
       ones += p->forced_mask[t];
     }
-    if (p->forced_mask[0] != 1 || ones != p->B) return fail(c, DIT_EINVAL, "forced mask needs m_0 = 1 and B ones");
+    if (p->forced_mask[0] != 1) return fail(c, DIT_EINVAL, "forced mask needs m_0 = 1");
+    if (p->policy != DIT_POLICY_THRESHOLD && ones != p->B)
+      return fail(c, DIT_EINVAL, "forced mask needs exactly B ones");
   }
   GateMLP gate;
-  TRY(parse_gate(c, gate_weights, gate_len, gate));
+  if (p->policy == DIT_POLICY_GATE) TRY(parse_gate(c, gate_weights, gate_len, gate));
   const auto t0 = std::chrono::steady_clock::now();
   dit_status st = run_sample(c, latent, text_emb, gate, *p, out);
   if (st != DIT_OK) hipStreamSynchronize(c->stream);
@@ -909,6 +993,7 @@ dit_status dit_cache_sample(dit_cache* c, float* latent, const void* text_emb, i
   dit_sample_params p{};
   p.T = T; p.B = B; p.sigmas = nullptr; p.shift = 1.0; p.tau = 0.5; p.guidance = 1.0;
   p.forced_mask = nullptr; p.indicator = DIT_INDICATOR_MODULATED;
+  p.policy = DIT_POLICY_GATE; p.delta = 0.0;
   return dit_cache_sample_ex(c, latent, text_emb, gate_weights, gate_len, &p, out);
 }
 

@@ -362,6 +362,37 @@ def make_gate_blob(widths=(8, 32, 16, 1), seed: int = 0, std: float = 0.3,
     return np.concatenate([np.asarray(head + z, np.float32), params])
 
 
+def make_branched_gate_blob(branches=((3, 8, 8), (3, 8, 8)), trunk=(16, 32, 1), seed: int = 0,
+                            std: float = 0.3, zscore=None) -> np.ndarray:
+    """Self-describing float32 blob of a branched gate (default: the Wan
+    gate shape of App. A.2, 785 parameters).
+
+    Layout: [-n, (k_j, widths_j) for each branch, k, trunk widths, zflag,
+    (mu[D], sd[D] if zflag), branch parameters in branch order, trunk
+    parameters], D = sum of the branch input widths; each network's
+    parameters are W_1, b_1, W_2, b_2, ... with W_l row-major
+    [d_l, d_{l-1}].
+    Parameters ~ N(0, std^2).  ``zscore`` = (mu, sd) arrays or None."""
+    branches = [tuple(int(w) for w in b) for b in branches]
+    trunk = tuple(int(w) for w in trunk)
+    n = sum(gate_param_count(b) for b in branches) + gate_param_count(trunk)
+    params = np.empty(n, np.float32)
+    _fill_normal(params, (seed, _GATE, 1), std, False)
+    head = [-float(len(branches))]
+    for b in branches + [trunk]:
+        head += [float(len(b))] + [float(w) for w in b]
+    d_in = sum(b[0] for b in branches)
+    if zscore is None:
+        head.append(0.0)
+        z = []
+    else:
+        mu, sd = (np.asarray(a, np.float32) for a in zscore)
+        assert mu.shape == (d_in,) and sd.shape == (d_in,)
+        head.append(1.0)
+        z = list(mu) + list(sd)
+    return np.concatenate([np.asarray(head + z, np.float32), params])
+
+
 def make_inputs(w: Workload):
     """(weights, latent, text, gate blob) of a workload, all seeded."""
     cfg = w.model

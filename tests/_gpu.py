@@ -51,21 +51,22 @@ def assert_bf16_close(got, ref, frac_exact=0.9, ulps=1, atol_rms=2.0 ** -10):
 
 
 def run_sampler(torch, w: synth.Workload, weights, x0, text, gate, *, T=None, B=None, forced=None,
-                tau=0.5, indicator="modulated", handle=None):
+                tau=0.5, indicator="modulated", handle=None, **kw):
     cfg = w.model
     h = handle or binding.DitCache(cfg, weights.blob)
     lat = dev(torch, x0.astype(np.float32))
     txt = dev(torch, text)
     sched = h.sample(lat, txt, gate, T or w.T, B or w.B, shift=w.shift, tau=tau,
-                     guidance=w.guidance, forced_mask=forced, indicator=indicator)
+                     guidance=w.guidance, forced_mask=forced, indicator=indicator, **kw)
     torch.cuda.synchronize()
     return lat.cpu().numpy().astype(np.float64), sched, h
 
 
-def check_schedule_against_oracle(sched, ores, margin=1e-3):
-    """Decisions agree wherever the gate logit is more than `margin` from the
-    threshold; counts are exact.  `ores` is the oracle replaying the device's
-    schedule, so both sides see the same history."""
+def check_schedule_against_oracle(sched, ores, margin=1e-3, cut=0.0):
+    """Decisions agree wherever the decision statistic (gate logit, or q_t of
+    the threshold rule) is more than `margin` from its cutoff `cut`; counts
+    are exact.  `ores` is the oracle replaying the device's schedule, so both
+    sides see the same history."""
     T = len(sched.full)
     assert sched.full[0] == 1
     assert int(sched.full.sum()) == int(ores.nfe)
@@ -74,5 +75,7 @@ def check_schedule_against_oracle(sched, ores, margin=1e-3):
             assert sched.forced[t] == 1
             continue
         z = ores.logit[t]
-        if abs(z) > margin:
-            assert sched.full[t] == (1 if z > 0 else 0), (t, z, sched.logit[t])
+        if np.isnan(z):
+            continue
+        if abs(z - cut) > margin:
+            assert sched.full[t] == (1 if z > cut else 0), (t, z, sched.logit[t])

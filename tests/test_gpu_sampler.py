@@ -20,19 +20,27 @@ TOL = {"f32": 1e-5, "bf16": 2e-2}
 SUM_TOL = {"f32": 1e-5, "bf16": 1e-3}
 
 
-def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5):
+def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5, gate=None, policy="gate", delta=0.0):
     torch = torch_cuda()
     w = synth.workload(name)
     cfg = w.model
-    weights, x0, text, gate = synth.make_inputs(w)
+    weights, x0, text, wgate = synth.make_inputs(w)
+    gate = wgate if gate is None else gate
     T = T or w.T
     B = B or w.B
-    x_gpu, sched, h = run_sampler(torch, w, weights, x0, text, gate, T=T, B=B, indicator=indicator, tau=tau)
+    pol = dict(policy=policy, delta=delta)
+    x_gpu, sched, h = run_sampler(torch, w, weights, x0, text, gate, T=T, B=B, indicator=indicator, tau=tau,
+                                  **pol)
     h.close()
-    assert sched.nfe == B and int(sched.full.sum()) == B and sched.full[0] == 1
+    if policy != "threshold":
+        assert sched.nfe == B and int(sched.full.sum()) == B
+    assert sched.full[0] == 1 and int(sched.full.sum()) == sched.nfe
     ores = oracle_sample(cfg, weights.tensors, gate, x0, text, T, B, shift=w.shift, tau=tau,
-                         guidance=w.guidance, forced_mask=sched.full, indicator=indicator)
-    check_schedule_against_oracle(sched, ores)
+                         guidance=w.guidance, forced_mask=sched.full, indicator=indicator, **pol)
+    if policy == "threshold":
+        check_schedule_against_oracle(sched, ores, margin=1e-2 * abs(delta), cut=delta)
+    else:
+        check_schedule_against_oracle(sched, ores)
     err = rel_l2(x_gpu, ores.x)
     assert err <= TOL[cfg.dtype], err
     ok = np.isfinite(ores.sums[1:])
@@ -40,8 +48,9 @@ def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5):
     np.testing.assert_allclose(sched.features[1:, :4], ores.features[1:, :4], rtol=1e-12)
     np.testing.assert_allclose(sched.features[1:, 4:], ores.features[1:, 4:], rtol=10 * SUM_TOL[cfg.dtype])
     gated = oracle_sample(cfg, weights.tensors, gate, x0, text, T, B, shift=w.shift, tau=tau,
-                          guidance=w.guidance, indicator=indicator)
-    if np.all(np.abs(ores.logit[1:]) > 1e-3):
+                          guidance=w.guidance, indicator=indicator, **pol)
+    stat = ores.logit[1:] - (delta if policy == "threshold" else 0.0)
+    if np.all(np.isnan(stat) | (np.abs(stat) > (1e-2 * abs(delta) if policy == "threshold" else 1e-3))):
         np.testing.assert_array_equal(sched.full, gated.full)
     return sched, ores, err
 
@@ -77,6 +86,40 @@ def test_budget_edges_tiny():
         parity("tiny", T=T, B=B)
 
 
+def test_paper_flux_gate_with_zscore():
+    """App. A.2's FLUX / Qwen gate shape 6-8-8-32-1 (449 parameters) with
+    z-scored inputs: reads f0..f5 only."""
+    mu = np.array([0.4, 0.5, 0.6, 2.0, 0.1, 0.05], np.float32)
+    sd = np.array([0.2, 0.3, 0.4, 1.5, 0.1, 0.05], np.float32)
+    gate = synth.make_gate_blob((6, 8, 8, 32, 1), seed=11, zscore=(mu, sd))
+    parity("tiny", gate=gate)
+    parity("small_bf16", gate=gate)
+
+
+def test_wan_branched_gate():
+    """App. A.2's Wan gate: two 3-8-8 branches (budget / trajectory state)
+    fused by 16-32-1, 785 parameters, z-scored inputs; on the video
+    cross-attention model."""
+    mu = np.array([0.3, 0.5, 0.6, 2.0, 0.1, 0.05], np.float32)
+    sd = np.array([0.1, 0.3, 0.4, 1.5, 0.1, 0.05], np.float32)
+    gate = synth.make_branched_gate_blob(seed=5, zscore=(mu, sd))
+    parity("tiny", gate=gate)
+    parity("small_cross_bf16", gate=gate)
+
+
+def test_static_policy():
+    from oracle import static_schedule
+    for name in ("tiny", "small_bf16"):
+        sched, _, _ = parity(name, policy="static", gate=np.zeros(0, np.float32))
+        np.testing.assert_array_equal(sched.full, static_schedule(int(sched.nfe), len(sched.full)))
+
+
+@pytest.mark.parametrize("name,delta", [("tiny", 0.05), ("small_bf16", 0.05), ("small_cfg_bf16", 0.07)])
+def test_threshold_policy(name, delta):
+    sched, ores, _ = parity(name, policy="threshold", delta=delta, gate=np.zeros(0, np.float32))
+    print(name, "threshold", delta, "nfe", sched.nfe, "schedule", sched.full.tolist())
+
+
 def test_forced_replay_and_determinism():
     torch = torch_cuda()
     w = synth.workload("small_bf16")
@@ -107,6 +150,15 @@ def test_error_paths_on_device():
     assert e.value.status == binding.DIT_EINVAL
     with pytest.raises(binding.DitError) as e:
         h.sample(lat, txt, gate, 5, 2, forced_mask=[0, 1, 1, 0, 0])
+    assert e.value.status == binding.DIT_EINVAL
+    bad_gate = synth.make_branched_gate_blob(seed=5)
+    bad_gate[10] = 15          # trunk input width != sum of branch outputs
+    for g in (bad_gate, bad_gate[:-1], None):
+        with pytest.raises(binding.DitError) as e:
+            h.sample(lat, txt, g, 5, 2)
+        assert e.value.status == binding.DIT_EINVAL
+    with pytest.raises(binding.DitError) as e:
+        h.sample(lat, txt, None, 5, 2, policy="threshold", delta=float("nan"))
     assert e.value.status == binding.DIT_EINVAL
     bad = lat.clone()
     bad[3, 2] = float("nan")

@@ -61,6 +61,68 @@ def test_gate_forward_vs_torch_sequential(widths, zs):
         assert math.isclose(gate.logit(f), ref, rel_tol=1e-12, abs_tol=1e-12)
 
 
+def _torch_mlp(blob, p, widths, last_relu):
+    mods = []
+    for i in range(1, len(widths)):
+        lin = torch.nn.Linear(widths[i - 1], widths[i]).double()
+        n = widths[i] * widths[i - 1]
+        with torch.no_grad():
+            lin.weight.copy_(torch.from_numpy(blob[p:p + n].astype(np.float64).reshape(widths[i], widths[i - 1])))
+            p += n
+            lin.bias.copy_(torch.from_numpy(blob[p:p + widths[i]].astype(np.float64)))
+            p += widths[i]
+        mods.append(lin)
+        if i < len(widths) - 1 or last_relu:
+            mods.append(torch.nn.ReLU())
+    return torch.nn.Sequential(*mods), p
+
+
+@pytest.mark.parametrize("zs", [False, True])
+def test_branched_gate_vs_torch_modules(zs):
+    """App. A.2 Wan gate: two 3->8->8 branches (budget state f0..f2 and
+    trajectory state f3..f5), concatenated, fused by 16->32->1."""
+    rng = np.random.default_rng(17)
+    z = None
+    if zs:
+        z = (rng.standard_normal(6).astype(np.float32), (0.5 + rng.random(6)).astype(np.float32))
+    blob = synth.make_branched_gate_blob(seed=3, zscore=z)
+    gate = parse_gate_blob(blob)
+    assert gate.n_params == json.load(open(GOLDEN))["gate_params_wan"]["value"]
+    assert gate.d_in == 6
+    # header: -2, (3; 3 8 8), (3; 3 8 8), (3; 16 32 1), zflag
+    assert list(blob[:14]) == [-2, 3, 3, 8, 8, 3, 3, 8, 8, 3, 16, 32, 1, float(zs)]
+    p = 14 + (12 if zs else 0)
+    b1, p = _torch_mlp(blob, p, (3, 8, 8), True)
+    b2, p = _torch_mlp(blob, p, (3, 8, 8), True)
+    trunk, p = _torch_mlp(blob, p, (16, 32, 1), False)
+    assert p == blob.size
+    for _ in range(20):
+        f = rng.standard_normal(8) * 2
+        u = f[:6]
+        if zs:
+            u = (u - z[0].astype(np.float64)) / z[1].astype(np.float64)
+        ut = torch.from_numpy(u).reshape(1, -1)
+        ref = float(trunk(torch.cat([b1(ut[:, :3]), b2(ut[:, 3:])], dim=1)).detach()[0, 0])
+        assert math.isclose(gate.logit(f), ref, rel_tol=1e-12, abs_tol=1e-12)
+
+
+def test_branched_gate_blob_rejects_bad_headers():
+    blob = synth.make_branched_gate_blob(seed=3)
+    with pytest.raises(ValueError):
+        parse_gate_blob(blob[:-1])
+    bad = blob.copy()
+    bad[10] = 15  # trunk input width != 8 + 8
+    with pytest.raises(ValueError):
+        parse_gate_blob(bad)
+    bad = blob.copy()
+    bad[0] = -2.5
+    with pytest.raises(ValueError):
+        parse_gate_blob(bad)
+    big = synth.make_branched_gate_blob(branches=((5, 8), (4, 8)), seed=3)
+    with pytest.raises(ValueError):  # 9 inputs > the 8 state features
+        parse_gate_blob(big)
+
+
 def test_gate_blob_rejects_bad_lengths():
     blob = synth.make_gate_blob((8, 32, 16, 1), seed=1)
     with pytest.raises(ValueError):
