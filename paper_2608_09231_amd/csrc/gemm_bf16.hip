@@ -12,6 +12,7 @@
 // M-grouped range of tiles (its own L2 sees the shared A rows / W columns).
 #include <stdlib.h>
 
+#include <type_traits>
 #include <utility>
 
 #include "common.h"
@@ -263,8 +264,23 @@ struct EpiLds {
     }
   }
 
-  // one 32-row slab: accumulators -> LDS -> 8-column row segments -> global
-  __device__ __forceinline__ void slab_pass(const f32x16_t (&a)[4], int i) {
+  // Residual values C[m][col .. col+3] of slab i (gated epilogue), loaded
+  // before any slab is staged so their latency overlaps the staging.
+  __device__ __forceinline__ void load_old(int i, uint2 (&old)[8][2]) const {
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      const int m = min(m_base + i * 32 + rq + 4 * p, P.M - 1);
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+        old[p][hh] = ok[hh] ? *(const uint2*)((const bf16_t*)P.C + (int64_t)m * P.ldc + col[hh]) : make_uint2(0, 0);
+    }
+  }
+
+  // One 32-row slab: accumulators -> LDS -> 8-column row segments -> global.
+  // Nothing waits on global memory here: a wave's LDS operations complete in
+  // order, so neither the read-back nor the next slab's writes need more
+  // than the wait for this wave's own slab writes.
+  __device__ __forceinline__ void slab_pass(const f32x16_t (&a)[4], int i, const uint2 (&old)[8][2]) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -273,7 +289,7 @@ struct EpiLds {
         const int c = (j * 32 + lrow) ^ (((row >> 2) & 1) << 5);
         slab[row * 128 + c] = a[j][r];
       }
-    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0) only
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
       const int row = rq + 4 * p;
@@ -315,40 +331,40 @@ struct EpiLds {
           } else {
             bf16_t* c = (bf16_t*)P.C + (int64_t)m * P.ldc + col[hh];
             if (gated) {
-              const uint2 old = *(const uint2*)c;
-              v[hh][0] = __uint_as_float(old.x << 16) + gv[hh][0] * v[hh][0];
-              v[hh][1] = __uint_as_float(old.x & 0xffff0000u) + gv[hh][1] * v[hh][1];
-              v[hh][2] = __uint_as_float(old.y << 16) + gv[hh][2] * v[hh][2];
-              v[hh][3] = __uint_as_float(old.y & 0xffff0000u) + gv[hh][3] * v[hh][3];
+              const uint2 o = old[p][hh];
+              v[hh][0] = __uint_as_float(o.x << 16) + gv[hh][0] * v[hh][0];
+              v[hh][1] = __uint_as_float(o.x & 0xffff0000u) + gv[hh][1] * v[hh][1];
+              v[hh][2] = __uint_as_float(o.y << 16) + gv[hh][2] * v[hh][2];
+              v[hh][3] = __uint_as_float(o.y & 0xffff0000u) + gv[hh][3] * v[hh][3];
             }
             *(uint2*)c = make_uint2(pack_bf16x2(v[hh][0], v[hh][1]), pack_bf16x2(v[hh][2], v[hh][3]));
           }
         }
       }
     }
-    __builtin_amdgcn_s_waitcnt(0);
   }
 };
 
-// LDS-staged epilogue for waves that own 128 output columns (WN == 128).
-// Per 32-row slab: the raw f32 accumulators go to this wave's 16 KB of LDS
-// (columns XOR 32 on rows with bit 2 set, so the two lane halves of a write
-// hit different banks); then lane l handles rows l/16 + 4p (p = 0..7) and
-// columns 4(l%16) + [0,4) and 64 + 4(l%16) + [0,4): bias, per-head RMS (a
-// head is the 16 lanes of one row: 4 shuffles), GELU / SiLU, gated
-// residual, and 8-byte stores that coalesce to 128 bytes per row.  Each slab
-// index is a compile-time constant so the accumulators stay in registers.
-// Requires N % 8 == 0, gelu_from and gap_at multiples of 4.
+// Runs the slab passes of a wave that owns TM x 32 rows and 128 columns;
+// with the gated residual, the old values of every slab (of one slab at a
+// time when TM > 2) are requested first.
+// Each slab index is a compile-time constant so the accumulators stay in
+// registers.
 template <int TM, size_t... Is>
 __device__ __forceinline__ void epilogue_lds_impl(EpiLds& e, f32x16_t (&acc)[TM][4], std::index_sequence<Is...>) {
-  (e.slab_pass(acc[Is], (int)Is), ...);
-}
-
-template <int TM>
-__device__ __forceinline__ void epilogue_lds(const Prob& P, f32x16_t (&acc)[TM][4], int m0, int n0, int wm,
-                                             int wn, int lrow, int lhalf, float* slab) {
-  EpiLds e(P, m0 + wm * TM * 32, n0 + wn * 128, lrow, lhalf, slab);
-  epilogue_lds_impl<TM>(e, acc, std::make_index_sequence<TM>{});
+  if constexpr (TM <= 2) {
+    uint2 old[TM][8][2];
+    if (e.gated) (e.load_old((int)Is, old[Is]), ...);
+    (e.slab_pass(acc[Is], (int)Is, old[Is]), ...);
+  } else {  // bounded registers: one slab's old values at a time
+    auto one = [&](auto i) {
+      constexpr int I = decltype(i)::value;
+      uint2 old[8][2];
+      if (e.gated) e.load_old(I, old);
+      e.slab_pass(acc[I], I, old);
+    };
+    (one(std::integral_constant<int, (int)Is>{}), ...);
+  }
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -366,6 +382,18 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// 16 bytes per lane from base + voff + soff (bytes, 32-bit offsets) into LDS
+// at dst + 16 lane: a raw buffer load with an LDS destination.  Offsets past
+// 4 GiB - 1 read zeros; the host admits this path only when every row of
+// the operand lies below that bound.
+__device__ __forceinline__ void buf_lds16(const void* base, lds_void_t* dst, uint32_t voff, uint32_t soff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)0xffffffffu, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
+#endif
 }
 
 // Direct-to-LDS pipeline (K % BK == 0): BK-deep slices of A and W are copied
@@ -410,32 +438,30 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
   const int wm = wave / WGN, wn = wave % WGN;
   const int lrow = lane & 31, lhalf = lane >> 5;
 
-  // per-lane source offsets in elements (fixed for the whole K loop; the
-  // buffers of one problem stay below 2^31 elements)
+  // per-lane source offsets in bytes (fixed for the whole K loop; the host
+  // admits this kernel only when they fit in 32 bits); the slice offset
+  // kt * BK * 2 travels in the scalar offset of the buffer load
   uint32_t aoff[A_INS], boff[B_INS];
 #pragma unroll
   for (int j = 0; j < A_INS; ++j) {
     const int row = ROWS_PER_INS * (wave * A_INS + j) + lane / CPR;
     const int c = (lane % CPR) ^ ((row / RPB) % CPR);
-    aoff[j] = (uint32_t)min(m0 + row, P.M - 1) * (uint32_t)P.lda + c * 8;
+    aoff[j] = ((uint32_t)min(m0 + row, P.M - 1) * (uint32_t)P.lda + c * 8) * 2u;
   }
 #pragma unroll
   for (int j = 0; j < B_INS; ++j) {
     const int row = ROWS_PER_INS * (wave * B_INS + j) + lane / CPR;
     const int c = (lane % CPR) ^ ((row / RPB) % CPR);
-    boff[j] = (uint32_t)min(n0 + row, P.N - 1) * (uint32_t)P.ldw + c * 8;
+    boff[j] = ((uint32_t)min(n0 + row, P.N - 1) * (uint32_t)P.ldw + c * 8) * 2u;
   }
   auto issue = [&](int kt) {
     char* sA = smem + (kt % STAGES) * STAGE;
     char* sB = sA + BM * BK_ * 2;
-    const bf16_t* Ab = P.A + kt * BK_;
-    const bf16_t* Bb = P.W + kt * BK_;
+    const uint32_t so = (uint32_t)kt * BK_ * 2;
 #pragma unroll
-    for (int j = 0; j < A_INS; ++j)
-      __builtin_amdgcn_global_load_lds((glb_void_t*)(Ab + aoff[j]), (lds_void_t*)(sA + (wave * A_INS + j) * 1024), 16, 0, 0);
+    for (int j = 0; j < A_INS; ++j) buf_lds16(P.A, (lds_void_t*)(sA + (wave * A_INS + j) * 1024), aoff[j], so);
 #pragma unroll
-    for (int j = 0; j < B_INS; ++j)
-      __builtin_amdgcn_global_load_lds((glb_void_t*)(Bb + boff[j]), (lds_void_t*)(sB + (wave * B_INS + j) * 1024), 16, 0, 0);
+    for (int j = 0; j < B_INS; ++j) buf_lds16(P.W, (lds_void_t*)(sB + (wave * B_INS + j) * 1024), boff[j], so);
   };
 
   f32x16_t acc[TM][TN];
@@ -445,8 +471,73 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  // the epilogue state (bias, gate, column map) is loaded before the K loop
+  [[maybe_unused]] EpiLds epi(P, m0 + wm * TM * 32, n0 + wn * 128, lrow, lhalf, (float*)smem + wave * (32 * 128));
 
   const int nk = P.K / BK_;
+  if constexpr (STAGES == 2 && BK_ == 64) {
+    // Two 64-deep slices in LDS, fragments double-buffered in registers: the
+    // LDS reads of substep s+1 (and, in substep 0, the copies of the next
+    // slice) are interleaved with the 8 MFMAs of substep s; one barrier per
+    // slice, the last iteration peeled so the loop body has no branch.
+    auto rd = [&](int kt, int s, bf16x8_t(&af)[TM], bf16x8_t(&bfr)[TN]) {
+      const char* sA = smem + (kt & 1) * STAGE;
+      const char* sB = sA + BM * BK_ * 2;
+      const int kc = 2 * s + lhalf;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int row = wm * WM + i * 32 + lrow;
+        af[i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sA + row * (2 * BK_) + ((kc ^ ((row / RPB) % CPR)) << 4)));
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int row = wn * WN + j * 32 + lrow;
+        bfr[j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sB + row * (2 * BK_) + ((kc ^ ((row / RPB) % CPR)) << 4)));
+      }
+    };
+    auto mm = [&](const bf16x8_t(&af)[TM], const bf16x8_t(&bfr)[TN]) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    };
+    // instruction-group order of one substep: MFMA / LDS-read pairs, then
+    // what is left of either; WithCopy adds one buffer copy to each pair
+    auto sched = [&](auto with_copy) {
+      constexpr bool WithCopy = decltype(with_copy)::value;
+      constexpr int NM = TM * TN, ND = TM + TN, NP = NM < ND ? NM : ND;
+#pragma unroll
+      for (int q = 0; q < NP; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        if constexpr (WithCopy) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+      }
+      if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
+      if constexpr (ND > NP) __builtin_amdgcn_sched_group_barrier(0x100, ND - NP, 0);
+    };
+    using copy_t = std::integral_constant<bool, true>;
+    using nocopy_t = std::integral_constant<bool, false>;
+    bf16x8_t a0[TM], b0[TN], a1[TM], b1[TN];
+    issue(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    rd(0, 0, a0, b0);
+    for (int kt = 0; kt < nk - 1; ++kt) {
+      issue(kt + 1);  // into the buffer of slice kt-1, which every wave has finished
+      rd(kt, 1, a1, b1); mm(a0, b0); sched(copy_t{});
+      rd(kt, 2, a0, b0); mm(a1, b1); sched(nocopy_t{});
+      rd(kt, 3, a1, b1); mm(a0, b0); sched(nocopy_t{});
+      mm(a1, b1);
+      wait_vmcnt<0>();  // this wave's copies of slice kt+1 have landed
+      __syncthreads();  // everyone's have, and every read of slice kt is done
+      rd(kt + 1, 0, a0, b0);
+    }
+    rd(nk - 1, 1, a1, b1); mm(a0, b0); sched(nocopy_t{});
+    rd(nk - 1, 2, a0, b0); mm(a1, b1); sched(nocopy_t{});
+    rd(nk - 1, 3, a1, b1); mm(a0, b0); sched(nocopy_t{});
+    mm(a1, b1);
+  } else {
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nk) issue(s);
@@ -480,10 +571,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
   }
+  }
   __syncthreads();  // all waves are done with the slices before the epilogue reuses LDS
   if constexpr (kLdsEpilogue<WN, NW, STAGES * STAGE>) {
-    float* slab = (float*)smem + wave * (32 * 128);
-    epilogue_lds<TM>(P, acc, m0, n0, wm, wn, lrow, lhalf, slab);
+    epilogue_lds_impl<TM>(epi, acc, std::make_index_sequence<TM>{});
   } else {
     epilogue<TM, TN, WM, WN>(P, acc, m0, n0, wm, wn, lrow, lhalf);
   }
@@ -557,8 +648,6 @@ struct Cfg {
    gemm_bf16_dma_kernel<BM, BN, WGM, WGN, BK_, ST>}
 const Cfg kCfgs[] = {
     DIT_DMA_CFG(256, 256, 4, 2, 64, 2, 1, 1.00f),
-    DIT_DMA_CFG(256, 256, 4, 2, 32, 4, 1, 0.95f),
-    DIT_DMA_CFG(256, 256, 2, 2, 64, 2, 1, 0.99f),
     DIT_DMA_CFG(256, 128, 4, 1, 64, 2, 1, 0.72f),
     DIT_DMA_CFG(128, 128, 4, 1, 64, 2, 2, 0.85f),
     DIT_DMA_CFG(32, 256, 1, 4, 64, 2, 2, 0.45f),
@@ -604,10 +693,15 @@ int pick_cfg(const GemmArgs* g, int n, int n_cu) {
     epi_ok &= g[i].gelu_from >= g[i].N || (g[i].gelu_from % 4) == 0;
     epi_ok &= g[i].gap == 0 || ((g[i].gap_at | g[i].gap) % 4) == 0;
   }
+  bool off32 = true;  // byte offsets of every A / W row fit the buffer loads' 32 bits
+  for (int i = 0; i < n; ++i) {
+    off32 &= ((uint64_t)(g[i].M - 1) * g[i].lda + g[i].K) * 2 <= 0xffffffffull;
+    off32 &= ((uint64_t)(g[i].N - 1) * g[i].ldw + g[i].K) * 2 <= 0xffffffffull;
+  }
   auto admits = [&](const Cfg& k) {
     if (rms && k.wn % 128) return false;
     if (!k.dma) return true;
-    if (!aligned || (k.lds_epi && !epi_ok)) return false;
+    if (!aligned || !off32 || (k.lds_epi && !epi_ok)) return false;
     for (int i = 0; i < n; ++i)
       if (g[i].K % k.bk) return false;
     return true;
