@@ -242,7 +242,10 @@ struct EpiLds {
   float* slab;
 
   __device__ __forceinline__ EpiLds(const Prob& P_, int m_base_, int ncol0_, int lrow_, int lhalf_, float* slab_)
-      : P(P_), m_base(m_base_), ncol0(ncol0_), lrow(lrow_), lhalf(lhalf_), slab(slab_) {
+      : P(P_), m_base(m_base_), ncol0(ncol0_), lrow(lrow_), lhalf(lhalf_), slab(slab_) {}
+
+  // Flags, column map, bias and gate values of this lane's 8 columns.
+  __device__ __forceinline__ void prep() {
     const int lane = lhalf * 32 + lrow;
     cq = lane & 15;
     rq = lane >> 4;
@@ -471,8 +474,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  // the epilogue state (bias, gate, column map) is loaded before the K loop
+  // The epilogue state (bias, gate, column map) is loaded before the K loop
+  // when registers allow (TM <= 2), so those loads are done when the tile is.
   [[maybe_unused]] EpiLds epi(P, m0 + wm * TM * 32, n0 + wn * 128, lrow, lhalf, (float*)smem + wave * (32 * 128));
+  if constexpr (kLdsEpilogue<WN, NW, STAGES * STAGE> && TM <= 2) epi.prep();
 
   const int nk = P.K / BK_;
   if constexpr (STAGES == 2 && BK_ == 64) {
@@ -502,19 +507,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     };
-    // instruction-group order of one substep: MFMA / LDS-read pairs, then
-    // what is left of either; WithCopy adds one buffer copy to each pair
+    // Instruction order of one substep, fixed by scheduling groups: one MFMA,
+    // then two LDS reads of the next substep (and, with WithCopy, two buffer
+    // copies of the next slice), repeated; then the remaining MFMAs.  A
+    // scheduling fence closes every substep, so the reads stay one substep
+    // ahead of the MFMAs that consume them (two fragment sets live).
     auto sched = [&](auto with_copy) {
       constexpr bool WithCopy = decltype(with_copy)::value;
-      constexpr int NM = TM * TN, ND = TM + TN, NP = NM < ND ? NM : ND;
+      constexpr int NM = TM * TN, ND = TM + TN, NG = (ND + 1) / 2;
+      static_assert(NM >= NG, "substep shape");
 #pragma unroll
-      for (int q = 0; q < NP; ++q) {
+      for (int q = 0; q < NG; ++q) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        if constexpr (WithCopy) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM read
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+        if constexpr (WithCopy) __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // VMEM read
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read
       }
-      if constexpr (NM > NP) __builtin_amdgcn_sched_group_barrier(0x008, NM - NP, 0);
-      if constexpr (ND > NP) __builtin_amdgcn_sched_group_barrier(0x100, ND - NP, 0);
+      if constexpr (NM > NG) __builtin_amdgcn_sched_group_barrier(0x008, NM - NG, 0);
+      __builtin_amdgcn_sched_barrier(0);
     };
     using copy_t = std::integral_constant<bool, true>;
     using nocopy_t = std::integral_constant<bool, false>;
@@ -574,6 +583,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
   }
   __syncthreads();  // all waves are done with the slices before the epilogue reuses LDS
   if constexpr (kLdsEpilogue<WN, NW, STAGES * STAGE>) {
+    if constexpr (TM > 2) epi.prep();
     epilogue_lds_impl<TM>(epi, acc, std::make_index_sequence<TM>{});
   } else {
     epilogue<TM, TN, WM, WN>(P, acc, m0, n0, wm, wn, lrow, lhalf);
