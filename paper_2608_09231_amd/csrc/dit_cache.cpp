@@ -372,7 +372,7 @@ dit_status alloc_workspace(dit_cache* c) {
     std::vector<float> one(H, 1.f);
     HIPCK(hipMemcpy(c->ones, one.data(), H * 4, hipMemcpyHostToDevice));
   }
-  c->max_partials = dit::indicator_partials(N);
+  c->max_partials = std::max(dit::indicator_partials(N), dit::reuse_indicator_partials(N));
   TRY(dalloc(c, &c->partials, (size_t)c->max_partials * 4 * sizeof(double)));
   HIPCK(hipHostMalloc((void**)&c->sums_host, 4 * sizeof(double), hipHostMallocMapped));
   HIPCK(hipHostGetDevicePointer((void**)&c->sums_dev, c->sums_host, 0));
@@ -781,7 +781,14 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
         sc0 = sh0 + H;
       }
     }
-    {
+    const bool fused = c->bf16 && dit::reuse_fused_fits(c->C, H);
+    if (fused) {
+      // embedding recomputed in LDS: reads m_{t-1} and m_{t_last} (once if equal), writes m_t
+      Scope sc(c, DIT_K_INDICATOR, (double)N * H * c->esz * (t == 0 ? 1 : (i_prev == i_last ? 2 : 3)));
+      HIPCK(dit::launch_reuse_indicator(latent, c->C, c->M.img_in.w, c->M.img_in.b, c->mbuf[i_new],
+                                        t ? c->mbuf[i_prev] : nullptr, t ? c->mbuf[i_last] : nullptr, N, H,
+                                        sh0, sc0, t ? c->partials : nullptr, c->sums_dev, nullptr, c->stream));
+    } else {
       Scope sc(c, DIT_K_INDICATOR, (double)N * H * c->esz * (t == 0 ? 2 : (i_prev == i_last ? 3 : 4)));
       TRY(typed(c, [&](auto* tp) {
         using Ty = std::remove_pointer_t<decltype(tp)>;
@@ -852,31 +859,45 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
 
     // (a4) full or reuse, (a5) final layer + Euler
     const float dsig = (float)(sig[t + 1] - sig[t]);
-    const bool fused_euler = !pair && proj_fits(c);
-    float* lat_f = fused_euler ? latent : nullptr;
-    for (int b = 0; b < c->nb; ++b) {
-      if (dec) {
-        TRY(full_stack(c, b, s));
-        const void* hout = c->cfg.n_cross ? c->X : sp(c, c->X, (size_t)c->Nt * H);
-        TRY(final_layer(c, b, hout, s, DIT_K_FULL_OTHER, lat_f, dsig));
-      } else {
-        {
-          // h_out = S(h + r) and the final adaLN in one pass over the rows
-          Scope sc(c, DIT_K_REUSE, 3.0 * N * H * c->esz);
-          const float* mf = s.modp[b] + (c->n_mod - 2 * H);
-          TRY(typed(c, [&](auto* tp) {
-            using Ty = std::remove_pointer_t<decltype(tp)>;
-            return dit::launch_add_ln_mod<Ty>((const Ty*)c->h, (const Ty*)sp(c, c->r, (size_t)b * N * H),
-                                              (Ty*)c->yf, N, H, mf, mf + H, c->stream);
-          }));
-        }
-        TRY(final_project(c, b, DIT_K_REUSE, lat_f, dsig));
+    if (fused && !dec) {
+      // h + r, final adaLN, projection, guidance and Euler in one pass per row tile
+      Scope sc(c, DIT_K_REUSE, (double)c->nb * N * H * c->esz);
+      const float* mf0 = s.modp[0] + (c->n_mod - 2 * H);
+      const float* mf1 = pair ? s.modp[1] + (c->n_mod - 2 * H) : nullptr;
+      HIPCK(dit::launch_reuse_final(latent, c->C, c->M.img_in.w, c->M.img_in.b, c->r, c->nb, c->M.fin.w,
+                                    c->M.fin.b, mf0, mf1, dsig, (float)p.guidance, N, H, c->stream));
+    } else {
+      if (fused) {  // the block stack's input h, bit-identical to the one the indicator used
+        Scope sc(c, DIT_K_FULL_OTHER, (double)N * H * c->esz);
+        HIPCK(dit::launch_reuse_indicator(latent, c->C, c->M.img_in.w, c->M.img_in.b, nullptr, nullptr, nullptr,
+                                          N, H, nullptr, nullptr, nullptr, nullptr, c->h, c->stream));
       }
-    }
-    if (!fused_euler) {
-      Scope sc(c, dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
-      HIPCK(dit::launch_euler(latent, c->vel, pair ? c->vel + (size_t)N * c->C : nullptr,
-                              (float)p.guidance, dsig, (int64_t)N * c->C, c->stream));
+      const bool fused_euler = !pair && proj_fits(c);
+      float* lat_f = fused_euler ? latent : nullptr;
+      for (int b = 0; b < c->nb; ++b) {
+        if (dec) {
+          TRY(full_stack(c, b, s));
+          const void* hout = c->cfg.n_cross ? c->X : sp(c, c->X, (size_t)c->Nt * H);
+          TRY(final_layer(c, b, hout, s, DIT_K_FULL_OTHER, lat_f, dsig));
+        } else {
+          {
+            // h_out = S(h + r) and the final adaLN in one pass over the rows
+            Scope sc(c, DIT_K_REUSE, 3.0 * N * H * c->esz);
+            const float* mf = s.modp[b] + (c->n_mod - 2 * H);
+            TRY(typed(c, [&](auto* tp) {
+              using Ty = std::remove_pointer_t<decltype(tp)>;
+              return dit::launch_add_ln_mod<Ty>((const Ty*)c->h, (const Ty*)sp(c, c->r, (size_t)b * N * H),
+                                                (Ty*)c->yf, N, H, mf, mf + H, c->stream);
+            }));
+          }
+          TRY(final_project(c, b, DIT_K_REUSE, lat_f, dsig));
+        }
+      }
+      if (!fused_euler) {
+        Scope sc(c, dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
+        HIPCK(dit::launch_euler(latent, c->vel, pair ? c->vel + (size_t)N * c->C : nullptr,
+                                (float)p.guidance, dsig, (int64_t)N * c->C, c->stream));
+      }
     }
     if (dec) {
       cnt += 1;

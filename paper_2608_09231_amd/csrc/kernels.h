@@ -60,6 +60,25 @@ hipError_t launch_indicator(const T* h, T* m_out, const T* m_prev, const T* m_la
                             int H, const float* sh, const float* sc, double* partials, double* out,
                             hipStream_t s);
 int indicator_partials(int rows);
+// out[0..3] = fixed-order float64 sum of n partial 4-vectors (out host-mapped).
+hipError_t launch_reduce_partials(const double* partials, int n, double* out, hipStream_t s);
+
+// Fused streaming kernels (bf16; C in {32, 64, 128}, H % 32 == 0): the
+// patch embedding h = S(S(x) W_in^T + b_in) is recomputed in LDS.
+bool reuse_fused_fits(int C, int H);
+int reuse_indicator_partials(int rows);
+// m_out = S(LN(h)(1 + sc) + sh) (m_out = h when sc == nullptr) and, with
+// partials != nullptr, the four relative-L1 sums against m_prev / m_last into
+// out[4]; with h_out != nullptr only h is written (to h_out).
+hipError_t launch_reuse_indicator(const float* x, int C, const void* W_in, const void* b_in, void* m_out,
+                                  const void* m_prev, const void* m_last, int rows, int H, const float* sh,
+                                  const float* sc, double* partials, double* out, void* h_out, hipStream_t s);
+// Reuse step of nb (1 or 2) branches: h_out = S(h + r_b), y = S(LN(h_out)(1 +
+// scale) + shift) with (shift, scale) = mod_b[0..H), mod_b[H..2H), v_b = y
+// W_out^T + b_out, v = v_0 (nb = 1) or v_1 + guidance (v_0 - v_1), x += dsig v.
+hipError_t launch_reuse_final(float* x, int C, const void* W_in, const void* b_in, const void* r, int nb,
+                              const void* W_out, const void* b_out, const float* mod0, const float* mod1,
+                              float dsig, float guidance, int rows, int H, hipStream_t s);
 // y = S(LN(S(a + b))(1+sc)+sh) per row (reuse-step final-layer input).
 template <typename T>
 hipError_t launch_add_ln_mod(const T* a, const T* b, T* out, int rows, int H, const float* sh,

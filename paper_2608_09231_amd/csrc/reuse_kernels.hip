@@ -1,0 +1,490 @@
+// Fused per-step kernels of the cached sampler's streaming path (bf16,
+// gfx950): the patch embedding is recomputed inside each kernel instead of
+// being stored, so a reuse step moves only what the method needs.
+//
+//  * reuse_indicator_kernel  (a1 + a2 of every step)
+//      h = S(S(x) W_in^T + b_in) for a tile of RR token rows, on MFMA into
+//      LDS; then per row m_t = S(LN(h)(1 + scale0) + shift0) is written and
+//      the relative-L1 sums against m_{t-1} and m_{t_last} accumulated
+//      (f64 partials per workgroup, reduced in a fixed order afterwards).
+//      With h_out != nullptr it writes h instead (the full step's block-stack
+//      input, bit-identical to the h the indicator saw).
+//  * reuse_final_kernel  (a4 reuse + a5)
+//      per branch: h_out = S(h + r), y = S(LN(h_out)(1 + scale_f) + shift_f)
+//      into LDS, v = y W_out^T + b_out on MFMA, guidance combine, and the
+//      Euler update x += dsigma v in place.
+// HBM traffic of a reuse step: read m_{t-1}, m_{t_last} (once if equal) and
+// r, write m_t, plus the latent (N x C f32) and the L2-resident embedding /
+// projection weights.
+#include <math.h>
+
+#include <type_traits>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace dit {
+namespace {
+
+constexpr int RR = 16;  // token rows per workgroup (the MFMA's 16 token lanes)
+constexpr int RW = 8;   // waves per workgroup
+constexpr int LPAD = 8; // bf16 elements of padding per LDS row (16 bytes)
+
+__device__ __forceinline__ void unpack8(const uint4& u, float (&v)[8]) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
+__device__ __forceinline__ uint4 pack8(const float (&v)[8]) {
+  return make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                    pack_bf16x2(v[6], v[7]));
+}
+
+// Streamed tensors (read or written once per step) bypass L2 retention so the
+// embedding and projection weights, re-read by every workgroup, stay cached.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_stream(const bf16_t* p) {
+  const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void st_stream(bf16_t* p, uint4 v) {
+  const u32x4_t w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, (u32x4_t*)p);
+}
+
+__device__ __forceinline__ void load_f8(const float* p, float (&m)[8]) {
+  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+  m[0] = a.x; m[1] = a.y; m[2] = a.z; m[3] = a.w; m[4] = b.x; m[5] = b.y; m[6] = b.z; m[7] = b.w;
+}
+
+// Copies n16 16-byte vectors global -> LDS with the whole workgroup; every
+// thread issues its loads (up to 8 in flight) before its stores.
+__device__ __forceinline__ void stage(const void* src, void* dst, int n16) {
+  constexpr int NT = 64 * RW, U = 4;
+  for (int i0 = threadIdx.x; i0 < n16; i0 += NT * U) {
+    uint4 v[U];
+    // indices clamped instead of tested: no branches, so all loads issue
+    // before the first store (clamped duplicates store the same value twice)
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = ((const uint4*)src)[min(i0 + u * NT, n16 - 1)];
+#pragma unroll
+    for (int u = 0; u < U; ++u) ((uint4*)dst)[min(i0 + u * NT, n16 - 1)] = v[u];
+  }
+}
+
+// h rows row0 .. row0 + RR - 1 into LDS (row stride ldl): the transposed
+// product h^T = W_in S(x)^T on 16x16x32 MFMAs, 16 h-columns per tile (bias
+// b_in read from its LDS copy bl); the
+// operand's 16 token lanes cover the RR rows (lanes past them repeat the
+// last valid row and are not stored).  Lane (lr, lq) ends with
+// h[row lr][16 j + 4 lq + i], i = 0..3: one 8-byte LDS store.
+template <int CK>
+__device__ __forceinline__ void embed_to_lds(const float* __restrict__ x, int C, const bf16_t* __restrict__ W,
+                                             const bf16_t* bl, int row0, int rows, int H, bf16_t* hl, int ldl,
+                                             int wave, int lane) {
+  const int lr = lane & 15, lq = lane >> 4;
+  const int xr = min(row0 + min(lr, RR - 1), rows - 1);
+  bf16x8_t xf[CK];
+#pragma unroll
+  for (int s = 0; s < CK; ++s) {
+    float v[8];
+    load_f8(x + (int64_t)xr * C + 32 * s + 8 * lq, v);
+    xf[s] = __builtin_bit_cast(bf16x8_t, pack8(v));
+  }
+  const bool store = lr < RR && row0 + lr < rows;
+  // W_in tiles stream from L2 in batches of EB, the next batch in flight
+  // while the current one is multiplied and stored
+  constexpr int EB = 4;
+  const int ntile = H / 16;  // tiles j = wave + RW * u
+  const int nu = (ntile - wave + RW - 1) / RW;
+  uint4 wcur[EB][CK], wnxt[EB][CK];
+  // every workgroup walks its tiles from a different start, so the CUs of an
+  // XCD do not all request the same L2 lines at the same time
+  const int rot = blockIdx.x % nu;
+  auto tile_of = [&](int u) { const int v = u + rot; return wave + RW * (v < nu ? v : v - nu); };
+  auto load_batch = [&](int u0, uint4 (&w)[EB][CK]) {
+#pragma unroll
+    for (int e = 0; e < EB; ++e) {
+      const int u = min(u0 + e, nu - 1);
+      const bf16_t* wp = W + (int64_t)(16 * tile_of(u) + lr) * C + 8 * lq;
+#pragma unroll
+      for (int s = 0; s < CK; ++s) w[e][s] = *(const uint4*)(wp + 32 * s);
+    }
+  };
+  load_batch(0, wcur);
+  for (int u0 = 0; u0 < nu; u0 += EB) {
+    if (u0 + EB < nu) load_batch(u0 + EB, wnxt);
+#pragma unroll
+    for (int e = 0; e < EB; ++e) {
+      if (u0 + e >= nu) break;
+      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < CK; ++s)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wcur[e][s]), xf[s], acc, 0, 0, 0);
+      if (store) {
+        const int n = 16 * tile_of(u0 + e) + 4 * lq;
+        const uint2 bb = *(const uint2*)(bl + n);
+        const float b0 = __uint_as_float(bb.x << 16), b1 = __uint_as_float(bb.x & 0xffff0000u);
+        const float b2 = __uint_as_float(bb.y << 16), b3 = __uint_as_float(bb.y & 0xffff0000u);
+        *(uint2*)(hl + lr * ldl + n) =
+            make_uint2(pack_bf16x2(acc[0] + b0, acc[1] + b1), pack_bf16x2(acc[2] + b2, acc[3] + b3));
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < EB; ++e)
+#pragma unroll
+      for (int s = 0; s < CK; ++s) wcur[e][s] = wnxt[e][s];
+  }
+}
+
+// LN statistics of one row held as MAXC 8-value chunks per lane (chunks
+// c = lane + 64 j < nch); two passes over registers, f32.
+template <int MAXC>
+__device__ __forceinline__ void row_stats(const float (&v)[MAXC][8], int nch, int H, int lane, float& mean,
+                                          float& rstd) {
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s += v[j][e];
+  mean = warp_sum(s) / (float)H;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < MAXC; ++j) {
+    if (lane + 64 * j < nch)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float d = v[j][e] - mean;
+        q += d * d;
+      }
+  }
+  rstd = rsqrtf(warp_sum(q) / (float)H + DIT_LN_EPS);
+}
+
+template <int CK, int MAXC>
+__global__ __launch_bounds__(64 * RW) void reuse_indicator_kernel(
+    const float* __restrict__ x, int C, const bf16_t* __restrict__ W_in, const bf16_t* __restrict__ b_in,
+    bf16_t* __restrict__ m_out, const bf16_t* __restrict__ m_prev, const bf16_t* __restrict__ m_last,
+    int rows, int H, const float* __restrict__ sh, const float* __restrict__ sc, double* __restrict__ partials,
+    bf16_t* __restrict__ h_out) {
+  // dynamic LDS: h tile [RR][H + LPAD] bf16, then b_in [H] bf16, then scale / shift [H] f32
+  extern __shared__ __attribute__((aligned(16))) bf16_t hl[];
+  __shared__ float red[RW][4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int row0 = blockIdx.x * RR;
+  const int ldl = H + LPAD, nch = H / 8;
+  constexpr int RPW = RR / RW;  // rows per wave
+  const bool sums = partials != nullptr && h_out == nullptr;
+  bf16_t* bl = hl + RR * ldl;
+  float* scl = (float*)(bl + H);
+  float* shl = scl + H;
+  stage(b_in, bl, H / 8);
+  if (sc && !h_out) {
+    stage(sc, scl, H / 4);
+    stage(sh, shl, H / 4);
+  }
+  const bool same = m_prev == m_last;
+
+  // the previous indicator rows stream in while the embedding runs
+  // (addresses clamped into the tensors so every load is unconditional and
+  // they all issue back to back; out-of-range chunks and rows are not used)
+  uint4 pv[RPW][MAXC], lv[RPW][MAXC];
+  if (sums) {
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) {
+      const int row = min(row0 + wave + RW * q, rows - 1);
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) {
+        const int c = min(lane + 64 * j, nch - 1);
+        pv[q][j] = ld_stream(m_prev + (int64_t)row * H + 8 * c);
+        if (!same) lv[q][j] = ld_stream(m_last + (int64_t)row * H + 8 * c);
+      }
+    }
+  }
+
+  __syncthreads();
+  embed_to_lds<CK>(x, C, W_in, bl, row0, rows, H, hl, ldl, wave, lane);
+  __syncthreads();
+
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    const int rr = wave + RW * q, row = row0 + rr;
+    if (row >= rows) break;
+    const bf16_t* src = hl + rr * ldl;
+    if (h_out) {  // block-stack input of a full step
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) {
+        const int c = lane + 64 * j;
+        if (c < nch) *(uint4*)(h_out + (int64_t)row * H + 8 * c) = *(const uint4*)(src + 8 * c);
+      }
+      continue;
+    }
+    float v[MAXC][8];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = lane + 64 * j;
+      unpack8(*(const uint4*)(src + 8 * min(c, nch - 1)), v[j]);
+      if (c >= nch)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[j][e] = 0.f;
+    }
+    float mean = 0.f, rstd = 1.f;
+    if (sc) row_stats<MAXC>(v, nch, H, lane, mean, rstd);
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = lane + 64 * j;
+      if (c >= nch) continue;
+      float y[8];
+      if (sc) {
+        float a[8], bsh[8];
+        load_f8(scl + 8 * c, a);
+        load_f8(shl + 8 * c, bsh);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = (v[j][e] - mean) * rstd * (1.f + a[e]) + bsh[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = v[j][e];
+      }
+      const uint4 packed = pack8(y);
+      st_stream(m_out + (int64_t)row * H + 8 * c, packed);
+      if (sums) {
+        float mv[8], p[8], l[8];
+        unpack8(packed, mv);  // the stored (rounded) m_t
+        unpack8(pv[q][j], p);
+        if (same) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) l[e] = p[e];
+        } else {
+          unpack8(lv[q][j], l);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          a0 += fabsf(mv[e] - p[e]);
+          a1 += fabsf(p[e]);
+          a2 += fabsf(mv[e] - l[e]);
+          a3 += fabsf(l[e]);
+        }
+      }
+    }
+  }
+  if (!sums) return;
+  a0 = warp_sum(a0); a1 = warp_sum(a1); a2 = warp_sum(a2); a3 = warp_sum(a3);
+  if (lane == 0) { red[wave][0] = a0; red[wave][1] = a1; red[wave][2] = a2; red[wave][3] = a3; }
+  __syncthreads();
+  if (threadIdx.x < 4) {
+    double s = 0.0;
+#pragma unroll
+    for (int w = 0; w < RW; ++w) s += (double)red[w][threadIdx.x];
+    partials[(int64_t)blockIdx.x * 4 + threadIdx.x] = s;
+  }
+}
+
+template <int CK, int MAXC, int NT>
+__global__ __launch_bounds__(64 * RW) void reuse_final_kernel(
+    float* __restrict__ x, int C, const bf16_t* __restrict__ W_in, const bf16_t* __restrict__ b_in,
+    const bf16_t* __restrict__ r, int nb, const bf16_t* __restrict__ W_out, const bf16_t* __restrict__ b_out,
+    const float* mod0, const float* mod1, float dsig, float guidance, int rows, int H) {
+  // dynamic LDS: h / y tile [RR][H + LPAD] bf16, then b_in [H] bf16, then scale / shift [H] f32
+  extern __shared__ __attribute__((aligned(16))) bf16_t hl[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lq = lane >> 4;
+  const int row0 = blockIdx.x * RR;
+  const int ldl = H + LPAD, nch = H / 8;
+  bf16_t* bl = hl + RR * ldl;
+  float* scl = (float*)(bl + H);
+  float* shl = scl + H;
+  constexpr int RPW = RR / RW;
+  static_assert(RW % NT == 0, "projection tiles divide the waves");
+  constexpr int KS = RW / NT;  // waves per projection tile
+  __shared__ float vpart[RW][64][4];
+  float vres[4] = {0.f, 0.f, 0.f, 0.f};
+
+  for (int b = 0; b < nb; ++b) {
+    const bf16_t* rb = r + (int64_t)b * rows * H;
+    const float* mod = b ? mod1 : mod0;
+    uint4 rv[RPW][MAXC];  // clamped, unconditional loads (see the indicator kernel)
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) {
+      const int row = min(row0 + wave + RW * q, rows - 1);
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) rv[q][j] = ld_stream(rb + (int64_t)row * H + 8 * min(lane + 64 * j, nch - 1));
+    }
+    if (b) __syncthreads();  // the previous branch's projection is done with the tile
+    if (b == 0) stage(b_in, bl, H / 8);
+    stage(mod + H, scl, H / 4);
+    stage(mod, shl, H / 4);
+    __syncthreads();
+    embed_to_lds<CK>(x, C, W_in, bl, row0, rows, H, hl, ldl, wave, lane);
+    __syncthreads();
+    // h_out = S(h + r), y = S(LN(h_out)(1 + sc) + sh), in place
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) {
+      const int rr = wave + RW * q, row = row0 + rr;
+      if (row >= rows) break;
+      bf16_t* src = hl + rr * ldl;
+      float v[MAXC][8];
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) {
+        const int c = lane + 64 * j;
+        float hv[8], rvv[8];
+        unpack8(*(const uint4*)(src + 8 * min(c, nch - 1)), hv);
+        unpack8(rv[q][j], rvv);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[j][e] = c < nch ? St<bf16_t>::rd(hv[e] + rvv[e]) : 0.f;
+      }
+      float mean, rstd;
+      row_stats<MAXC>(v, nch, H, lane, mean, rstd);
+#pragma unroll
+      for (int j = 0; j < MAXC; ++j) {
+        const int c = lane + 64 * j;
+        if (c >= nch) continue;
+        float a[8], bsh[8], y[8];
+        load_f8(scl + 8 * c, a);
+        load_f8(shl + 8 * c, bsh);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = (v[j][e] - mean) * rstd * (1.f + a[e]) + bsh[e];
+        *(uint4*)(src + 8 * c) = pack8(y);
+      }
+    }
+    __syncthreads();
+    // v^T = W_out y^T: lane (lr, lq) of tile j ends with v[row lr][16 j + 4 lq + i].
+    // KS waves share a tile, each a contiguous K range; partial sums meet in
+    // LDS and are added in wave order.
+    {
+      const int j = wave % NT, part = wave / NT;
+      const int ks = H / 32, per = ks / KS;  // H % (32 KS) == 0 (checked on the host)
+      const int s0 = part * per;
+      const int rot = (blockIdx.x * 8) % per;  // staggered start, as in the embedding
+      auto ks_of = [&](int q) { const int v = q + rot; return s0 + (v < per ? v : v - per); };
+      const bf16_t* wp = W_out + (int64_t)(16 * j + lr) * H + 8 * lq;
+      const bf16_t* yp = hl + lr * ldl + 8 * lq;
+      f32x4_t acc[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      constexpr int PB = 8;  // k-steps per batch of W_out loads
+      uint4 wb[PB], wn[PB];
+#pragma unroll
+      for (int u = 0; u < PB; ++u) wb[u] = *(const uint4*)(wp + 32 * ks_of(min(u, per - 1)));
+      for (int s = 0; s < per; s += PB) {
+        if (s + PB < per)
+#pragma unroll
+          for (int u = 0; u < PB; ++u) wn[u] = *(const uint4*)(wp + 32 * ks_of(min(s + PB + u, per - 1)));
+#pragma unroll
+        for (int u = 0; u < PB; ++u) {
+          if (s + u >= per) break;
+          acc[u & 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8_t, wb[u]), __builtin_bit_cast(bf16x8_t, *(const uint4*)(yp + 32 * ks_of(s + u))),
+              acc[u & 3], 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < PB; ++u) wb[u] = wn[u];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) vpart[wave][lane][i] = (acc[0][i] + acc[1][i]) + (acc[2][i] + acc[3][i]);
+    }
+    __syncthreads();
+    if (wave < NT) {
+      const uint2 bb = *(const uint2*)(b_out + 16 * wave + 4 * lq);
+      const float bias[4] = {__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
+                             __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xffff0000u)};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float vb = vpart[wave][lane][i];
+#pragma unroll
+        for (int p = 1; p < KS; ++p) vb += vpart[wave + NT * p][lane][i];
+        vb += bias[i];
+        // guidance: v = v_u + g (v_c - v_u), branch 0 conditional, branch 1 unconditional
+        vres[i] = b == 0 ? vb : vb + guidance * (vres[i] - vb);
+      }
+    }
+  }
+  // Euler update in place
+  if (wave < NT && row0 + lr < rows) {
+    float4* xp = (float4*)(x + (int64_t)(row0 + lr) * C + 16 * wave + 4 * lq);
+    float4 xv = *xp;
+    xv.x += dsig * vres[0];
+    xv.y += dsig * vres[1];
+    xv.z += dsig * vres[2];
+    xv.w += dsig * vres[3];
+    *xp = xv;
+  }
+}
+
+template <typename F>
+hipError_t dispatch_reuse(int C, int H, F f) {
+  const int per_lane = (H / 8 + 63) / 64;
+  auto with_c = [&](auto ck) -> hipError_t {
+    if (per_lane <= 2) return f(ck, std::integral_constant<int, 2>());
+    if (per_lane <= 4) return f(ck, std::integral_constant<int, 4>());
+    if (per_lane <= 6) return f(ck, std::integral_constant<int, 6>());
+    if (per_lane <= 10) return f(ck, std::integral_constant<int, 10>());
+    return hipErrorInvalidValue;
+  };
+  if (C == 32) return with_c(std::integral_constant<int, 1>());
+  if (C == 64) return with_c(std::integral_constant<int, 2>());
+  if (C == 128) return with_c(std::integral_constant<int, 4>());
+  return hipErrorInvalidValue;
+}
+
+// Dynamic LDS of both kernels: the row tile plus staged b_in, scale, shift.
+size_t dyn_lds(int H) { return (size_t)RR * (H + LPAD) * 2 + (size_t)H * 2 + (size_t)H * 8; }
+
+// Lets a kernel take `bytes` of dynamic LDS (beyond the 64 KB default).
+hipError_t allow_lds(const void* kern, size_t bytes) {
+  return hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
+}  // namespace
+
+bool reuse_fused_fits(int C, int H) {
+  if (C != 32 && C != 64 && C != 128) return false;
+  const int ks_waves = RW / (C / 16);  // waves sharing one projection tile
+  return H >= 16 * RW && H % (32 * ks_waves) == 0 && (H / 8 + 63) / 64 <= 10 &&
+         dyn_lds(H) + sizeof(float) * RW * 64 * 4 <= 160 * 1024;
+}
+
+int reuse_indicator_partials(int rows) { return (rows + RR - 1) / RR; }
+
+hipError_t launch_reuse_indicator(const float* x, int C, const void* W_in, const void* b_in, void* m_out,
+                                  const void* m_prev, const void* m_last, int rows, int H, const float* sh,
+                                  const float* sc, double* partials, double* out, void* h_out, hipStream_t s) {
+  if (!reuse_fused_fits(C, H) || rows < 1) return hipErrorInvalidValue;
+  const int nblk = reuse_indicator_partials(rows);
+  const size_t lds = dyn_lds(H);
+  hipError_t e = dispatch_reuse(C, H, [&](auto ck, auto mc) {
+    auto kern = reuse_indicator_kernel<decltype(ck)::value, decltype(mc)::value>;
+    hipError_t a = allow_lds((const void*)kern, lds);
+    if (a != hipSuccess) return a;
+    hipLaunchKernelGGL(kern, dim3(nblk), dim3(64 * RW), lds, s, x, C, (const bf16_t*)W_in, (const bf16_t*)b_in,
+                       (bf16_t*)m_out, (const bf16_t*)m_prev, (const bf16_t*)m_last, rows, H, sh, sc,
+                       h_out ? nullptr : partials, (bf16_t*)h_out);
+    return hipGetLastError();
+  });
+  if (e != hipSuccess || !partials || h_out) return e;
+  return launch_reduce_partials(partials, nblk, out, s);
+}
+
+hipError_t launch_reuse_final(float* x, int C, const void* W_in, const void* b_in, const void* r, int nb,
+                              const void* W_out, const void* b_out, const float* mod0, const float* mod1,
+                              float dsig, float guidance, int rows, int H, hipStream_t s) {
+  if (!reuse_fused_fits(C, H) || rows < 1 || nb < 1 || nb > 2) return hipErrorInvalidValue;
+  const int nblk = (rows + RR - 1) / RR;
+  const size_t lds = dyn_lds(H);
+  return dispatch_reuse(C, H, [&](auto ck, auto mc) {
+    constexpr int CK = decltype(ck)::value;
+    auto kern = reuse_final_kernel<CK, decltype(mc)::value, 2 * CK>;
+    hipError_t a = allow_lds((const void*)kern, lds);
+    if (a != hipSuccess) return a;
+    hipLaunchKernelGGL(kern, dim3(nblk), dim3(64 * RW), lds, s, x, C, (const bf16_t*)W_in, (const bf16_t*)b_in,
+                       (const bf16_t*)r, nb, (const bf16_t*)W_out, (const bf16_t*)b_out, mod0, mod1, dsig,
+                       guidance, rows, H);
+    return hipGetLastError();
+  });
+}
+
+}  // namespace dit

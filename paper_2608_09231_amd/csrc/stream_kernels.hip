@@ -418,7 +418,11 @@ hipError_t launch_indicator(const T* h, T* m_out, const T* m_prev, const T* m_la
     return hipGetLastError();
   });
   if (e != hipSuccess || !partials) return e;
-  hipLaunchKernelGGL(reduce_partials_kernel, dim3(1), dim3(256), 0, s, partials, nb, out);
+  return launch_reduce_partials(partials, nb, out, s);
+}
+
+hipError_t launch_reduce_partials(const double* partials, int n, double* out, hipStream_t s) {
+  hipLaunchKernelGGL(reduce_partials_kernel, dim3(1), dim3(256), 0, s, partials, n, out);
   return hipGetLastError();
 }
 
