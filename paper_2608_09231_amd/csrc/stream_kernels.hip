@@ -54,22 +54,29 @@ template <> struct Chunk<float> {
 };
 
 // One wave per row: the row lives in registers as MAXC chunks per lane.
-template <typename T, int MAXC>
+// FULL: the row is exactly 64 MAXC chunks, so no lane needs a range test
+// (tests become branches, and a load behind a branch waits for the previous
+// one).
+template <typename T, int MAXC, bool FULL = false>
 struct RowRegs {
   static constexpr int E = Chunk<T>::E;
   float v[MAXC][E];
   int nch;
+  // Every chunk load is issued unconditionally (chunk index clamped into the
+  // row) so they all stay in flight together; chunks past the row end are
+  // then zeroed.  A tested load would become a branch with a wait behind it.
   __device__ __forceinline__ void load(const T* x, int H, int lane) {
     nch = H / E;
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-      const int c = lane + 64 * j;
-      if (c < nch) Chunk<T>::load(x + c * E, v[j]);
-      else
+    for (int j = 0; j < MAXC; ++j) Chunk<T>::load(x + cl(lane + 64 * j) * E, v[j]);
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j)
+      if (!ok(lane + 64 * j))
 #pragma unroll
         for (int e = 0; e < E; ++e) v[j][e] = 0.f;
-    }
   }
+  __device__ __forceinline__ int cl(int c) const { return FULL || c < nch ? c : nch - 1; }
+  __device__ __forceinline__ bool ok(int c) const { return FULL || c < nch; }
   // LN statistics over H values (two passes over registers)
   __device__ __forceinline__ void stats(int H, int lane, float& mean, float& rstd) const {
     float s = 0.f;
@@ -81,7 +88,7 @@ struct RowRegs {
     float q = 0.f;
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
-      if (lane + 64 * j < nch)
+      if (ok(lane + 64 * j))
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           const float d = v[j][e] - mean;
@@ -101,7 +108,7 @@ __device__ __forceinline__ void load_mod(const float* p, float (&m)[4]) {
   m[0] = a.x; m[1] = a.y; m[2] = a.z; m[3] = a.w;
 }
 
-template <typename T, int MAXC>
+template <typename T, int MAXC, bool FULL>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, int64_t ldx,
                                                     T* __restrict__ out, int64_t ldo, int rows, int H,
                                                     int split, const float* sh0, const float* sc0,
@@ -110,29 +117,32 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, in
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
-  RowRegs<T, MAXC> r;
+  RowRegs<T, MAXC, FULL> r;
   r.load(x + (int64_t)row * ldx, H, lane);
   float mean, rstd;
   r.stats(H, lane, mean, rstd);
   const float* sh = row < split ? sh0 : sh1;
   const float* sc = row < split ? sc0 : sc1;
   T* o = out + (int64_t)row * ldo;
+  if (sc) {
 #pragma unroll
-  for (int j = 0; j < MAXC; ++j) {
-    const int c = lane + 64 * j;
-    if (c < r.nch) {
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = lane + 64 * j, cc = r.cl(c);  // clamped: loads without branches
+      float y[E], a[E], b[E];
+      load_mod(sc + cc * E, a);
+      load_mod(sh + cc * E, b);
+#pragma unroll
+      for (int e = 0; e < E; ++e) y[e] = (r.v[j][e] - mean) * rstd * (1.f + a[e]) + b[e];
+      if (r.ok(c)) Chunk<T>::store(o + c * E, y);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = lane + 64 * j;
       float y[E];
-      if (sc) {
-        float a[E], b[E];
-        load_mod(sc + c * E, a);
-        load_mod(sh + c * E, b);
 #pragma unroll
-        for (int e = 0; e < E; ++e) y[e] = (r.v[j][e] - mean) * rstd * (1.f + a[e]) + b[e];
-      } else {
-#pragma unroll
-        for (int e = 0; e < E; ++e) y[e] = (r.v[j][e] - mean) * rstd;
-      }
-      Chunk<T>::store(o + c * E, y);
+      for (int e = 0; e < E; ++e) y[e] = (r.v[j][e] - mean) * rstd;
+      if (r.ok(c)) Chunk<T>::store(o + c * E, y);
     }
   }
 }
@@ -145,7 +155,7 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, in
 constexpr int IRW = 1;
 constexpr int IROWS = 4 * IRW;  // rows per workgroup
 
-template <typename T, int MAXC>
+template <typename T, int MAXC, bool FULL>
 __global__ __launch_bounds__(256) void indicator_kernel(const T* __restrict__ h, T* __restrict__ m,
                                                        const T* __restrict__ mp,
                                                        const T* __restrict__ ml, int rows, int H,
@@ -160,36 +170,34 @@ __global__ __launch_bounds__(256) void indicator_kernel(const T* __restrict__ h,
     const int row = (blockIdx.x * 4 + wave) * IRW + i;
     if (row >= rows) break;
     const int64_t base = (int64_t)row * H;
-    RowRegs<T, MAXC> r;
+    RowRegs<T, MAXC, FULL> r;
     r.load(h + base, H, lane);
     uint4 pv[MAXC], lv[MAXC];
     if (mp) {
 #pragma unroll
       for (int j = 0; j < MAXC; ++j) {
-        const int c = lane + 64 * j;
-        if (c < r.nch) {
-          pv[j] = *(const uint4*)(mp + base + c * E);
-          if (!same) lv[j] = *(const uint4*)(ml + base + c * E);
-        }
+        const int cc = r.cl(lane + 64 * j);  // clamped: loads without branches
+        pv[j] = *(const uint4*)(mp + base + cc * E);
+        if (!same) lv[j] = *(const uint4*)(ml + base + cc * E);
       }
     }
     float mean = 0.f, rstd = 1.f;
     if (sc) r.stats(H, lane, mean, rstd);
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
-      const int c = lane + 64 * j;
-      if (c >= r.nch) continue;
+      const int c = lane + 64 * j, cc = r.cl(c);
       float y[E];
       if (sc) {
         float a[E], b[E];
-        load_mod(sc + c * E, a);
-        load_mod(sh + c * E, b);
+        load_mod(sc + cc * E, a);
+        load_mod(sh + cc * E, b);
 #pragma unroll
         for (int e = 0; e < E; ++e) y[e] = St<T>::rd((r.v[j][e] - mean) * rstd * (1.f + a[e]) + b[e]);
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e) y[e] = r.v[j][e];
       }
+      if (!r.ok(c)) continue;
       Chunk<T>::store(m + base + c * E, y);
       if (mp) {
         float p[E], l[E];
@@ -247,7 +255,7 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(const double* __re
 
 // Reuse-step final-layer input: y = S(LN(S(a + b)) (1 + sc) + sh), one wave
 // per row (a = h, b = cached residual r).
-template <typename T, int MAXC>
+template <typename T, int MAXC, bool FULL>
 __global__ __launch_bounds__(256) void add_ln_mod_kernel(const T* __restrict__ a, const T* __restrict__ b,
                                                         T* __restrict__ out, int rows, int H,
                                                         const float* sh, const float* sc) {
@@ -256,31 +264,27 @@ __global__ __launch_bounds__(256) void add_ln_mod_kernel(const T* __restrict__ a
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
   const int64_t base = (int64_t)row * H;
-  RowRegs<T, MAXC> r;
+  RowRegs<T, MAXC, FULL> r;
   r.load(a + base, H, lane);
+  float q[MAXC][E];
 #pragma unroll
-  for (int j = 0; j < MAXC; ++j) {
-    const int c = lane + 64 * j;
-    if (c < r.nch) {
-      float q[E];
-      Chunk<T>::load(b + base + c * E, q);
+  for (int j = 0; j < MAXC; ++j) Chunk<T>::load(b + base + r.cl(lane + 64 * j) * E, q[j]);
 #pragma unroll
-      for (int e = 0; e < E; ++e) r.v[j][e] = St<T>::rd(r.v[j][e] + q[e]);
-    }
-  }
+  for (int j = 0; j < MAXC; ++j)
+    if (r.ok(lane + 64 * j))
+#pragma unroll
+      for (int e = 0; e < E; ++e) r.v[j][e] = St<T>::rd(r.v[j][e] + q[j][e]);
   float mean, rstd;
   r.stats(H, lane, mean, rstd);
 #pragma unroll
   for (int j = 0; j < MAXC; ++j) {
-    const int c = lane + 64 * j;
-    if (c < r.nch) {
-      float y[E], s1[E], s2[E];
-      load_mod(sc + c * E, s1);
-      load_mod(sh + c * E, s2);
+    const int c = lane + 64 * j, cc = r.cl(c);
+    float y[E], s1[E], s2[E];
+    load_mod(sc + cc * E, s1);
+    load_mod(sh + cc * E, s2);
 #pragma unroll
-      for (int e = 0; e < E; ++e) y[e] = (r.v[j][e] - mean) * rstd * (1.f + s1[e]) + s2[e];
-      Chunk<T>::store(out + base + c * E, y);
-    }
+    for (int e = 0; e < E; ++e) y[e] = (r.v[j][e] - mean) * rstd * (1.f + s1[e]) + s2[e];
+    if (r.ok(c)) Chunk<T>::store(out + base + c * E, y);
   }
 }
 
@@ -382,15 +386,25 @@ inline int grid_for(int64_t n, int bs) {
 
 }  // namespace
 
+// Calls f(MAXC, FULL) for the smallest MAXC in the set with 64 MAXC >= H / E
+// chunks; FULL when the row is exactly 64 MAXC chunks.
 template <typename T, typename F>
 hipError_t dispatch_maxc(int H, F f) {
   constexpr int E = Chunk<T>::E;
-  const int per_lane = (H / E + 63) / 64;
-  if (per_lane <= 2) return f(std::integral_constant<int, 2>());
-  if (per_lane <= 4) return f(std::integral_constant<int, 4>());
-  if (per_lane <= 8) return f(std::integral_constant<int, 8>());
-  if (per_lane <= 16) return f(std::integral_constant<int, 16>());
-  if (per_lane <= 32) return f(std::integral_constant<int, 32>());
+  const int nch = H / E;
+  const int per_lane = (nch + 63) / 64;
+  auto go = [&](auto mc) -> hipError_t {
+    if (nch == 64 * decltype(mc)::value) return f(mc, std::true_type());
+    return f(mc, std::false_type());
+  };
+  if (per_lane <= 2) return go(std::integral_constant<int, 2>());
+  if (per_lane <= 4) return go(std::integral_constant<int, 4>());
+  if (per_lane <= 6) return go(std::integral_constant<int, 6>());
+  if (per_lane <= 8) return go(std::integral_constant<int, 8>());
+  if (per_lane <= 10) return go(std::integral_constant<int, 10>());
+  if (per_lane <= 12) return go(std::integral_constant<int, 12>());
+  if (per_lane <= 16) return go(std::integral_constant<int, 16>());
+  if (per_lane <= 32) return go(std::integral_constant<int, 32>());
   return hipErrorInvalidValue;
 }
 
@@ -400,8 +414,8 @@ hipError_t launch_ln_mod(const T* x, int64_t ldx, T* out, int64_t ldo, int rows,
                          hipStream_t s) {
   if (H % Chunk<T>::E) return hipErrorInvalidValue;
   if (rows <= 0) return hipSuccess;
-  return dispatch_maxc<T>(H, [&](auto mc) {
-    hipLaunchKernelGGL((ln_mod_kernel<T, decltype(mc)::value>), dim3((rows + 3) / 4), dim3(256), 0, s, x,
+  return dispatch_maxc<T>(H, [&](auto mc, auto fl) {
+    hipLaunchKernelGGL((ln_mod_kernel<T, decltype(mc)::value, decltype(fl)::value>), dim3((rows + 3) / 4), dim3(256), 0, s, x,
                        ldx, out, ldo, rows, H, split, sh0, sc0, sh1, sc1);
     return hipGetLastError();
   });
@@ -412,8 +426,8 @@ hipError_t launch_indicator(const T* h, T* m_out, const T* m_prev, const T* m_la
                             const float* sh, const float* sc, double* partials, double* out, hipStream_t s) {
   if (H % Chunk<T>::E) return hipErrorInvalidValue;
   const int nb = (rows + IROWS - 1) / IROWS;
-  hipError_t e = dispatch_maxc<T>(H, [&](auto mc) {
-    hipLaunchKernelGGL((indicator_kernel<T, decltype(mc)::value>), dim3(nb), dim3(256), 0, s, h, m_out,
+  hipError_t e = dispatch_maxc<T>(H, [&](auto mc, auto fl) {
+    hipLaunchKernelGGL((indicator_kernel<T, decltype(mc)::value, decltype(fl)::value>), dim3(nb), dim3(256), 0, s, h, m_out,
                        m_prev, m_last, rows, H, sh, sc, partials);
     return hipGetLastError();
   });
@@ -431,8 +445,9 @@ hipError_t launch_add_ln_mod(const T* a, const T* b, T* out, int rows, int H, co
                              const float* sc, hipStream_t s) {
   if (H % Chunk<T>::E) return hipErrorInvalidValue;
   if (rows <= 0) return hipSuccess;
-  return dispatch_maxc<T>(H, [&](auto mc) {
-    hipLaunchKernelGGL((add_ln_mod_kernel<T, decltype(mc)::value>), dim3((rows + 3) / 4), dim3(256), 0, s,
+  return dispatch_maxc<T>(H, [&](auto mc, auto fl) {
+    hipLaunchKernelGGL((add_ln_mod_kernel<T, decltype(mc)::value, decltype(fl)::value>), dim3((rows + 3) / 4),
+                       dim3(256), 0, s,
                        a, b, out, rows, H, sh, sc);
     return hipGetLastError();
   });
