@@ -237,6 +237,10 @@ def main():
             "attention_frac_bf16_peak": attn_tflops / PEAK_BF16_TFLOPS,
             "reuse_path_gbs": reuse_gbs,
             "indicator_gbs": ind_gbs,
+            # streaming kernels together (indicator every step + reuse steps): algorithmic
+            # bytes over their event time, against the 8 TB/s HBM peak
+            "streaming_hbm_frac": ((work["indicator"] + work["reuse"]) / ((ms["indicator"] + ms["reuse"]) * 1e-3)
+                                   / (PEAK_HBM_GBS * 1e9)) if (ms["indicator"] + ms["reuse"]) else 0.0,
             "ms_per_sample_by_class": {k: v / max(args.steps, 1) for k, v in ms.items()},
             "host_gate_ms_per_sample": st["host_gate_ms"] / max(args.steps, 1),
             "full_steps": st["full_steps"], "reuse_steps": st["reuse_steps"],
