@@ -40,6 +40,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 from . import dit
+from . import unipc
 from .gate import parse_gate_blob, tau_logit
 from .numerics import round_f32, storage_to_f64
 
@@ -99,7 +100,7 @@ class SampleResult:
 
 def sample(cfg, weights, gate_blob, x0, text, T, B, *, sigmas=None, shift=1.0,
            tau=0.5, guidance=1.0, forced_mask=None, indicator="modulated",
-           trace=False, gate_fn=None, policy="gate", delta=0.0):
+           trace=False, gate_fn=None, policy="gate", delta=0.0, solver="euler"):
     """Run one cached sample.
 
     cfg       model config (attributes as in the workload registry)
@@ -110,11 +111,19 @@ def sample(cfg, weights, gate_blob, x0, text, T, B, *, sigmas=None, shift=1.0,
     gate_fn   optional callable(features) -> logit, for tests
     policy    "gate" | "static" | "threshold" (module docstring); delta is
               the threshold rule's cutoff
+    solver    "euler" (step 5 above) or "unipc": the UniPC-2 predictor-corrector
+              of ``oracle.unipc`` on the data prediction m_t = S32(x_t - sigma_t v)
+              (the network always sees the uncorrected x_t; the corrector then
+              refines x_t, and the predictor steps from the corrected sample)
     """
     if not (1 <= B <= T):
         raise ValueError("budget must satisfy 1 <= B <= T")
     if policy not in ("gate", "static", "threshold"):
         raise ValueError("unknown policy")
+    if solver not in ("euler", "unipc"):
+        raise ValueError("unknown solver")
+    ords = unipc.orders(T)
+    hist, x_last = [], None
     mu = static_schedule(B, T) if policy == "static" else None
     P = dit.Params(cfg, weights)
     rs = P.rs
@@ -195,8 +204,18 @@ def sample(cfg, weights, gate_blob, x0, text, T, B, *, sigmas=None, shift=1.0,
             m_last = m_t
             acc = 0.0
         v = v_b[0] if nb == 1 else v_b[1] + guidance * (v_b[0] - v_b[1])
-        dsig = float(np.float32(sigmas[t + 1] - sigmas[t]))
-        x = round_f32(x + dsig * v)
+        if solver == "euler":
+            dsig = float(np.float32(sigmas[t + 1] - sigmas[t]))
+            x = round_f32(x + dsig * v)
+        else:
+            m = round_f32(x - sigmas[t] * v)
+            if t > 0:
+                x = round_f32(unipc.correct(x_last, hist[-1], hist[-2] if t > 1 else None, m, sigmas[t - 1],
+                                            sigmas[t - 2] if t > 1 else 1.0, sigmas[t], ords[t - 1]))
+            hist.append(m)
+            x_last = x
+            x = round_f32(unipc.predict(x, m, hist[-2] if t > 0 else None, sigmas[t],
+                                        sigmas[t - 1] if t > 0 else 1.0, sigmas[t + 1], ords[t]))
         m_prev = m_t
         if t == 0:
             m_last = m_t

@@ -198,3 +198,40 @@ def test_tiny_workload_runs_and_spends_budget():
     res = sample(wl.model, w.tensors, gate, x0, text, wl.T, wl.B, shift=wl.shift)
     assert res.nfe == wl.B and res.full[0] == 1
     assert np.all(np.isfinite(res.x))
+
+
+@pytest.mark.parametrize("cfg", [NANO, NANO_CROSS], ids=lambda c: c.name)
+def test_unipc_zero_dit_is_exact(cfg):
+    """UniPC integrates the constant velocity b_out exactly: x_T = x_0 - b_out."""
+    w, x0, text = inputs(cfg)
+    for k, v in w.tensors.items():
+        v[...] = 0
+    bout = np.linspace(-1, 1, cfg.in_channels).astype(np.float32)
+    w.tensors["final.b"][...] = bout
+    res = sample(cfg, w.tensors, gate_for(cfg), x0, text, 9, 4, shift=3.0, solver="unipc")
+    np.testing.assert_allclose(res.x, x0.astype(np.float64) - bout, atol=2e-6)
+
+
+@pytest.mark.parametrize("cfg", [NANO, NANO_BF16], ids=lambda c: c.name)
+def test_unipc_full_budget_equals_standalone_unipc(cfg):
+    """B = T: the sampler's UniPC wiring equals the standalone UniPC loop with a
+    network call per step (same f32 storage points)."""
+    from oracle.unipc import integrate
+    w, x0, text = inputs(cfg)
+    T = 7
+    res = sample(cfg, w.tensors, gate_for(cfg), x0, text, T, T, shift=3.0, solver="unipc")
+    P = dit.Params(cfg, w.tensors)
+    sig = sigma_schedule(T, 3.0)
+    t64 = storage_to_f64(text[0], cfg.dtype)
+    txt = dit.text_in(P, t64)
+    mods = dit.mod_table(P, dit.vec_table(P, sig[:T], t64))
+    step = {"t": 0}
+
+    def velocity(x, s):
+        t = step["t"]
+        assert s == sig[t]
+        step["t"] += 1
+        h = dit.patch_embed(P, x)
+        return dit.final_layer(P, dit.block_stack(P, h, txt, mods[t]), mods[t])
+
+    np.testing.assert_array_equal(res.x, integrate(velocity, x0, sig, rnd=round_f32))
