@@ -175,7 +175,7 @@ def main():
 
     def one():
         lat.copy_(lat0)
-        return h.sample(lat, txt, gate, w.T, w.B, shift=w.shift, guidance=w.guidance)
+        return h.sample(lat, txt, gate, w.T, w.B, shift=w.shift, guidance=w.guidance, solver=w.solver)
 
     for i in range(args.warmup):
         s = one()
@@ -217,7 +217,7 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic (seeded N(0,1) latent and text embeddings, N(0,0.02) random-init weights, N(0,0.3) gate)",
-        "config": {"workload": cfg.name, "T": w.T, "B": w.B, "blocks": f"{cfg.n_double} double + {cfg.n_single} single",
+        "config": {"workload": cfg.name, "T": w.T, "B": w.B, "solver": w.solver, "blocks": f"{cfg.n_double} double + {cfg.n_single} single",
                    "hidden": cfg.hidden, "heads": cfg.heads, "img_tokens": cfg.n_img, "txt_tokens": cfg.n_txt,
                    "batch": cfg.batch, "gate": "-".join(map(str, w.gate_widths))},
         "roofline": {

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define DIT_ABI_VERSION 2
+#define DIT_ABI_VERSION 3
 #define DIT_N_FEATURES 8
 
 typedef enum dit_status {
@@ -116,6 +116,16 @@ typedef struct dit_model_config {
  *              The gate blob is not read (may be NULL). */
 enum { DIT_POLICY_GATE = 0, DIT_POLICY_STATIC = 1, DIT_POLICY_THRESHOLD = 2 };
 
+/* Step rule applied to the network's velocity v_t at every step.
+ *   EULER  x_{t+1} = x_t + (sigma_{t+1} - sigma_t) v_t.
+ *   UNIPC  UniPC-2 predictor-corrector (Zhao et al. 2023; the Wan sampler of
+ *          Sec. 4.1) on the data prediction m_t = x_t - sigma_t v_t with
+ *          B(h) = e^h - 1, lambda = log((1 - sigma) / sigma): the network sees
+ *          x_t, the corrector then refines x_t with m_t, and the predictor
+ *          steps from the corrected sample.  Orders: min(2, i + 1, T - i) for
+ *          the predictor of step i; the corrector of step i uses step i-1's. */
+enum { DIT_SOLVER_EULER = 0, DIT_SOLVER_UNIPC = 1 };
+
 typedef struct dit_sample_params {
   int32_t T;                    /* steps, >= 1 */
   int32_t B;                    /* full evaluations, 1 <= B <= T */
@@ -128,6 +138,7 @@ typedef struct dit_sample_params {
   int32_t indicator;            /* DIT_INDICATOR_MODULATED (default) or DIT_INDICATOR_PATCH */
   int32_t policy;               /* DIT_POLICY_GATE (default), _STATIC or _THRESHOLD */
   double delta;                 /* DIT_POLICY_THRESHOLD's cutoff on q_t */
+  int32_t solver;               /* DIT_SOLVER_EULER (default) or DIT_SOLVER_UNIPC */
 } dit_sample_params;
 
 /* Per-step record, host arrays owned by the caller (each may be NULL

@@ -22,8 +22,9 @@ STATUS_NAMES = {0: "DIT_OK", -1: "DIT_EINVAL", -2: "DIT_ENOMEM", -3: "DIT_EHIP",
 DTYPE_F32, DTYPE_BF16 = 0, 1
 INDICATOR_MODULATED, INDICATOR_PATCH = 0, 1
 EPI_STORE, EPI_F32, EPI_GATED_RES, EPI_SILU = 0, 1, 2, 4
-ABI_VERSION = 2
+ABI_VERSION = 3
 POLICIES = {"gate": 0, "static": 1, "threshold": 2}
+SOLVERS = {"euler": 0, "unipc": 1}
 N_FEATURES = 8
 K_CLASSES = ["gemm", "attn", "indicator", "reuse", "full_other", "once"]
 
@@ -43,7 +44,7 @@ class SampleParamsC(C.Structure):
     _fields_ = [("T", C.c_int32), ("B", C.c_int32), ("sigmas", C.POINTER(C.c_double)),
                 ("shift", C.c_double), ("tau", C.c_double), ("guidance", C.c_double),
                 ("forced_mask", C.POINTER(C.c_uint8)), ("indicator", C.c_int32),
-                ("policy", C.c_int32), ("delta", C.c_double)]
+                ("policy", C.c_int32), ("delta", C.c_double), ("solver", C.c_int32)]
 
 
 class ScheduleC(C.Structure):
@@ -165,11 +166,12 @@ class DitCache:
 
     def sample(self, latent, text_emb, gate_blob, T, B, *, sigmas=None, shift=1.0, tau=0.5,
                guidance=1.0, forced_mask=None, indicator="modulated", policy="gate",
-               delta=0.0) -> Schedule:
+               delta=0.0, solver="euler") -> Schedule:
         """latent: torch f32 cuda [N, C] (in place); text_emb: torch cuda
         storage-dtype [batch, N_t, ctx] (bf16 workloads: int16/uint16 bits
         or torch.bfloat16); policy "gate" | "static" | "threshold" (the
-        latter two do not read gate_blob, which may be None)."""
+        latter two do not read gate_blob, which may be None); solver
+        "euler" | "unipc"."""
         gate = np.ascontiguousarray(gate_blob if gate_blob is not None else [], np.float32)
         full = np.zeros(T, np.uint8)
         logit = np.zeros(T, np.float32)
@@ -188,7 +190,7 @@ class DitCache:
                           float(shift), float(tau), float(guidance),
                           fm.ctypes.data_as(C.POINTER(C.c_uint8)) if fm is not None else None,
                           INDICATOR_PATCH if indicator == "patch" else INDICATOR_MODULATED,
-                          POLICIES[policy], float(delta))
+                          POLICIES[policy], float(delta), SOLVERS[solver])
         st = _lib.dit_cache_sample_ex(self._h, C.c_void_p(latent.data_ptr()),
                                       C.c_void_p(text_emb.data_ptr()),
                                       gate.ctypes.data_as(C.c_void_p) if gate.size else None, gate.size,

@@ -92,6 +92,8 @@ struct dit_cache {
   void* vt = nullptr;      // bf16 [heads, 128, round_up(L, 64)]
   void* yf = nullptr;      // [N, H] final-layer input
   float* vel = nullptr;    // f32 [nb, N, C]
+  float* x_last = nullptr; // f32 [N, C]: UniPC's corrected sample of the previous step
+  float* mh[3] = {nullptr, nullptr, nullptr};  // f32 [N, C]: UniPC data predictions (rotating)
   void* txt = nullptr;     // [nb, Nt, H]
   void* ctxkv = nullptr;   // [Nt, 2H] cross-attention k | v
   void* vt2 = nullptr;     // bf16 [heads, 128, round_up(Nt, 64)]
@@ -362,6 +364,8 @@ dit_status alloc_workspace(dit_cache* c) {
   if (c->bf16) TRY(dalloc(c, &c->vt, (size_t)c->cfg.heads * 128 * rup(L, 64) * 2));
   TRY(dalloc(c, &c->yf, (size_t)N * H * e));
   TRY(dalloc(c, &c->vel, (size_t)c->nb * N * c->C * 4));
+  TRY(dalloc(c, &c->x_last, (size_t)N * c->C * 4));
+  for (auto& m : c->mh) TRY(dalloc(c, &m, (size_t)N * c->C * 4));
   TRY(dalloc(c, &c->txt, (size_t)c->nb * Nt * H * e));
   if (c->cfg.n_cross) {
     TRY(dalloc(c, &c->ctxkv, (size_t)Nt * 2 * H * e));
@@ -732,6 +736,75 @@ dit_status prepare(dit_cache* c, const void* text_emb, const std::vector<double>
   return DIT_OK;
 }
 
+// ---------------------------------------------------------------- UniPC
+// lambda = log(alpha / sigma) with alpha = 1 - sigma; +-inf at sigma = 0 / 1.
+double unipc_lambda(double sg) {
+  if (sg >= 1.0) return -INFINITY;
+  if (sg <= 0.0) return INFINITY;
+  return std::log(1.0 - sg) - std::log(sg);
+}
+
+// Step sigma_s -> sigma_t: B = e^{-h} - 1 and b_1 = phi_1 / B, b_2 = 2 phi_2 / B
+// (phi_1 = B / (-h) - 1, phi_2 = phi_1 / (-h) - 1/2); h = +inf gives B = -1,
+// b_1 = b_2 = 1, the exact limits.
+struct UniStep { double h, B, b1, b2; };
+UniStep unipc_step(double ss, double st) {
+  const double h = unipc_lambda(st) - unipc_lambda(ss);
+  if (std::isinf(h)) return {INFINITY, -1.0, 1.0, 1.0};
+  const double hh = -h, B = std::expm1(hh);
+  const double phi1 = B / hh - 1.0, phi2 = phi1 / hh - 0.5;
+  return {h, B, phi1 / B, 2.0 * phi2 / B};
+}
+
+// r = (lambda_p - lambda_s) / h, -inf (its term vanishes) through sigma = 1.
+double unipc_ratio(double sp, double ss, double h) {
+  const double lp = unipc_lambda(sp);
+  if (std::isinf(lp) || std::isinf(h)) return -INFINITY;
+  return (lp - unipc_lambda(ss)) / h;
+}
+
+// Coefficients of step t: corrector of x_t (t >= 1, order of step t-1's
+// predictor) and predictor of x_{t+1} (order min(2, t + 1, T - t)).
+dit::UniCoef unipc_coef(const std::vector<double>& sig, int t, int T) {
+  auto ord = [&](int i) { return std::min(2, std::min(i + 1, T - i)); };
+  dit::UniCoef k{};
+  if (t > 0) {
+    const double ss = sig[t - 1], st = sig[t], sp = t > 1 ? sig[t - 2] : 1.0;
+    const UniStep u = unipc_step(ss, st);
+    const double a = 1.0 - st;
+    double cx = st / ss, cs = -a * u.B, cp = 0.0, ct;
+    if (ord(t - 1) == 1) {
+      ct = -a * u.B * 0.5;
+    } else {
+      const double r = unipc_ratio(sp, ss, u.h);
+      if (std::isinf(r)) {
+        ct = -a * u.B * u.b1;
+      } else {
+        const double rho1 = (u.b1 - u.b2) / (1.0 - r), rhot = u.b1 - rho1;
+        cp = -a * u.B * rho1 / r;
+        cs -= cp;
+        ct = -a * u.B * rhot;
+      }
+    }
+    cs -= ct;  // the corrector's terms are differences against m_{t-1}
+    k.corr = 1;
+    k.cx = (float)cx; k.cs = (float)cs; k.cp = (float)cp; k.ct = (float)ct;
+  }
+  const double ss = sig[t], st = sig[t + 1];
+  const UniStep u = unipc_step(ss, st);
+  const double a = 1.0 - st;
+  double pt = -a * u.B, pp = 0.0;
+  if (ord(t) == 2) {
+    const double r = unipc_ratio(sig[t - 1], ss, u.h);
+    if (!std::isinf(r)) {
+      pp = -a * u.B * 0.5 / r;
+      pt -= pp;
+    }
+  }
+  k.px = (float)(st / ss); k.pt = (float)pt; k.pp = (float)pp;
+  return k;
+}
+
 dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const GateMLP& gate,
                       const dit_sample_params& p, dit_schedule* out) {
   const int T = p.T, B = p.B;
@@ -857,22 +930,24 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
     if (out->sums)
       for (int k = 0; k < 4; ++k) out->sums[(size_t)t * 4 + k] = sums[k];
 
-    // (a4) full or reuse, (a5) final layer + Euler
+    // (a4) full or reuse, (a5) final layer + step rule
     const float dsig = (float)(sig[t + 1] - sig[t]);
+    const bool unipc = p.solver == DIT_SOLVER_UNIPC;
     if (fused && !dec) {
       // h + r, final adaLN, projection, guidance and Euler in one pass per row tile
       Scope sc(c, DIT_K_REUSE, (double)c->nb * N * H * c->esz);
       const float* mf0 = s.modp[0] + (c->n_mod - 2 * H);
       const float* mf1 = pair ? s.modp[1] + (c->n_mod - 2 * H) : nullptr;
       HIPCK(dit::launch_reuse_final(latent, c->C, c->M.img_in.w, c->M.img_in.b, c->r, c->nb, c->M.fin.w,
-                                    c->M.fin.b, mf0, mf1, dsig, (float)p.guidance, N, H, c->stream));
+                                    c->M.fin.b, mf0, mf1, dsig, (float)p.guidance, N, H,
+                                    unipc ? c->vel : nullptr, c->stream));
     } else {
       if (fused) {  // the block stack's input h, bit-identical to the one the indicator used
         Scope sc(c, DIT_K_FULL_OTHER, (double)N * H * c->esz);
         HIPCK(dit::launch_reuse_indicator(latent, c->C, c->M.img_in.w, c->M.img_in.b, nullptr, nullptr, nullptr,
                                           N, H, nullptr, nullptr, nullptr, nullptr, c->h, c->stream));
       }
-      const bool fused_euler = !pair && proj_fits(c);
+      const bool fused_euler = !pair && proj_fits(c) && !unipc;
       float* lat_f = fused_euler ? latent : nullptr;
       for (int b = 0; b < c->nb; ++b) {
         if (dec) {
@@ -893,11 +968,24 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
           TRY(final_project(c, b, DIT_K_REUSE, lat_f, dsig));
         }
       }
-      if (!fused_euler) {
+      if (!fused_euler && !unipc) {
         Scope sc(c, dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
         HIPCK(dit::launch_euler(latent, c->vel, pair ? c->vel + (size_t)N * c->C : nullptr,
                                 (float)p.guidance, dsig, (int64_t)N * c->C, c->stream));
       }
+    }
+    if (unipc) {
+      // the guidance pair's two velocities are combined here; the fused reuse
+      // kernel has already combined them
+      const bool vpair = pair && !(fused && !dec);
+      const dit::UniCoef k = unipc_coef(sig, t, T);
+      float* m_t = c->mh[t % 3];
+      const float* m_s = t >= 1 ? c->mh[(t + 2) % 3] : nullptr;
+      const float* m_p = (t >= 2 && k.cp != 0.f) ? c->mh[(t + 1) % 3] : nullptr;
+      Scope sc(c, dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
+      HIPCK(dit::launch_unipc(latent, c->vel, vpair ? c->vel + (size_t)N * c->C : nullptr, (float)p.guidance,
+                              (float)sig[t], c->x_last, (k.pp != 0.f || k.corr) ? m_s : nullptr, m_p, m_t, k,
+                              (int64_t)N * c->C, c->stream));
     }
     if (dec) {
       cnt += 1;
@@ -986,6 +1074,7 @@ dit_status dit_cache_sample_ex(dit_cache* c, float* latent, const void* text_emb
   if (!p->sigmas && !(p->shift > 0.0)) return fail(c, DIT_EINVAL, "shift must be > 0");
   if (p->policy != DIT_POLICY_GATE && p->policy != DIT_POLICY_STATIC && p->policy != DIT_POLICY_THRESHOLD)
     return fail(c, DIT_EINVAL, "bad policy");
+  if (p->solver != DIT_SOLVER_EULER && p->solver != DIT_SOLVER_UNIPC) return fail(c, DIT_EINVAL, "bad solver");
   if (p->policy == DIT_POLICY_THRESHOLD && std::isnan(p->delta))
     return fail(c, DIT_EINVAL, "threshold delta is NaN");
   if (p->forced_mask) {
@@ -1014,7 +1103,7 @@ dit_status dit_cache_sample(dit_cache* c, float* latent, const void* text_emb, i
   dit_sample_params p{};
   p.T = T; p.B = B; p.sigmas = nullptr; p.shift = 1.0; p.tau = 0.5; p.guidance = 1.0;
   p.forced_mask = nullptr; p.indicator = DIT_INDICATOR_MODULATED;
-  p.policy = DIT_POLICY_GATE; p.delta = 0.0;
+  p.policy = DIT_POLICY_GATE; p.delta = 0.0; p.solver = DIT_SOLVER_EULER;
   return dit_cache_sample_ex(c, latent, text_emb, gate_weights, gate_len, &p, out);
 }
 
@@ -1023,7 +1112,8 @@ void dit_cache_destroy(dit_cache* c) {
   if (c->stream) hipStreamSynchronize(c->stream);
   free_per_sample(c);
   void* ps[] = {c->wdev, c->xs, c->h, c->mbuf[0], c->mbuf[1], c->mbuf[2], c->r, c->X, c->A, c->Y, c->vt,
-                c->yf, c->vel, c->txt, c->ctxkv, c->vt2, c->ones, c->partials};
+                c->yf, c->vel, c->txt, c->ctxkv, c->vt2, c->ones, c->partials, c->x_last, c->mh[0],
+                c->mh[1], c->mh[2]};
   for (void* p : ps)
     if (p) hipFree(p);
   if (c->sums_host) hipHostFree(c->sums_host);

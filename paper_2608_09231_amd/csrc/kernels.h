@@ -76,9 +76,11 @@ hipError_t launch_reuse_indicator(const float* x, int C, const void* W_in, const
 // Reuse step of nb (1 or 2) branches: h_out = S(h + r_b), y = S(LN(h_out)(1 +
 // scale) + shift) with (shift, scale) = mod_b[0..H), mod_b[H..2H), v_b = y
 // W_out^T + b_out, v = v_0 (nb = 1) or v_1 + guidance (v_0 - v_1), x += dsig v.
+// With vout != nullptr the combined v is written there (f32 [rows, C]) and x
+// is left unchanged (the step rule runs afterwards).
 hipError_t launch_reuse_final(float* x, int C, const void* W_in, const void* b_in, const void* r, int nb,
                               const void* W_out, const void* b_out, const float* mod0, const float* mod1,
-                              float dsig, float guidance, int rows, int H, hipStream_t s);
+                              float dsig, float guidance, int rows, int H, float* vout, hipStream_t s);
 // y = S(LN(S(a + b))(1+sc)+sh) per row (reuse-step final-layer input).
 template <typename T>
 hipError_t launch_add_ln_mod(const T* a, const T* b, T* out, int rows, int H, const float* sh,
@@ -87,6 +89,15 @@ hipError_t launch_add_ln_mod(const T* a, const T* b, T* out, int rows, int H, co
 template <typename T>
 hipError_t launch_add(const T* a, const T* b, T* out, int64_t n, float sign, hipStream_t s);
 // x += dsigma * v (batch 1) or x += dsigma * (v_u + g (v_c - v_u)).
+// Coefficients of one UniPC step (corrector of x_t, predictor of x_{t+1}).
+struct UniCoef {
+  int corr;
+  float cx, cs, cp, ct;  // x_c = cx x_last + cs m_{t-1} + cp m_{t-2} + ct m_t
+  float px, pt, pp;      // x_{t+1} = px x_c + pt m_t + pp m_{t-1}
+};
+hipError_t launch_unipc(float* x, const float* v_c, const float* v_u, float g, float sig_t, float* x_last,
+                        const float* m_s, const float* m_p, float* m_t, const UniCoef& k, int64_t n,
+                        hipStream_t s);
 hipError_t launch_euler(float* x, const float* v_c, const float* v_u, float g, float dsigma,
                         int64_t n, hipStream_t s);
 // latent f32 -> storage type.

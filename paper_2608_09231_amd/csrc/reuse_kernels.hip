@@ -288,7 +288,7 @@ template <int CK, int MAXC, int NT>
 __global__ __launch_bounds__(64 * RW) void reuse_final_kernel(
     float* __restrict__ x, int C, const bf16_t* __restrict__ W_in, const bf16_t* __restrict__ b_in,
     const bf16_t* __restrict__ r, int nb, const bf16_t* __restrict__ W_out, const bf16_t* __restrict__ b_out,
-    const float* mod0, const float* mod1, float dsig, float guidance, int rows, int H) {
+    const float* mod0, const float* mod1, float dsig, float guidance, int rows, int H, float* __restrict__ vout) {
   // dynamic LDS: h / y tile [RR][H + LPAD] bf16, then b_in [H] bf16, then scale / shift [H] f32
   extern __shared__ __attribute__((aligned(16))) bf16_t hl[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -403,8 +403,10 @@ __global__ __launch_bounds__(64 * RW) void reuse_final_kernel(
       }
     }
   }
-  // Euler update in place
-  if (wave < NT && row0 + lr < rows) {
+  // Euler update in place, or v handed to the step rule
+  if (wave < NT && row0 + lr < rows && vout) {
+    *(float4*)(vout + (int64_t)(row0 + lr) * C + 16 * wave + 4 * lq) = make_float4(vres[0], vres[1], vres[2], vres[3]);
+  } else if (wave < NT && row0 + lr < rows) {
     float4* xp = (float4*)(x + (int64_t)(row0 + lr) * C + 16 * wave + 4 * lq);
     float4 xv = *xp;
     xv.x += dsig * vres[0];
@@ -471,7 +473,7 @@ hipError_t launch_reuse_indicator(const float* x, int C, const void* W_in, const
 
 hipError_t launch_reuse_final(float* x, int C, const void* W_in, const void* b_in, const void* r, int nb,
                               const void* W_out, const void* b_out, const float* mod0, const float* mod1,
-                              float dsig, float guidance, int rows, int H, hipStream_t s) {
+                              float dsig, float guidance, int rows, int H, float* vout, hipStream_t s) {
   if (!reuse_fused_fits(C, H) || rows < 1 || nb < 1 || nb > 2) return hipErrorInvalidValue;
   const int nblk = (rows + RR - 1) / RR;
   const size_t lds = dyn_lds(H);
@@ -482,7 +484,7 @@ hipError_t launch_reuse_final(float* x, int C, const void* W_in, const void* b_i
     if (a != hipSuccess) return a;
     hipLaunchKernelGGL(kern, dim3(nblk), dim3(64 * RW), lds, s, x, C, (const bf16_t*)W_in, (const bf16_t*)b_in,
                        (const bf16_t*)r, nb, (const bf16_t*)W_out, (const bf16_t*)b_out, mod0, mod1, dsig,
-                       guidance, rows, H);
+                       guidance, rows, H, vout);
     return hipGetLastError();
   });
 }

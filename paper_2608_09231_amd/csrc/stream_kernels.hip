@@ -315,6 +315,33 @@ __global__ void euler_kernel(float* __restrict__ x, const float* __restrict__ vc
   }
 }
 
+// One UniPC step per element (coefficients from the host, see UniCoef):
+// v = v_c or v_u + g (v_c - v_u); m_t = x_t - sigma_t v (stored);
+// corrector x_c = cx x_last + cs m_s + cp m_p + ct m_t (or x_t at step 0),
+// stored as the new x_last; predictor x_{t+1} = px x_c + pt m_t + pp m_s.
+// m_s = m_{t-1}, m_p = m_{t-2} (nullptr where the coefficient is 0).
+__global__ void unipc_kernel(float* __restrict__ x, const float* __restrict__ vc, const float* __restrict__ vu,
+                             float g, float sig_t, float* __restrict__ x_last, const float* __restrict__ m_s,
+                             const float* __restrict__ m_p, float* __restrict__ m_t, UniCoef k, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    float v = vc[i];
+    if (vu) v = vu[i] + g * (v - vu[i]);
+    const float xv = x[i];
+    const float m = xv - sig_t * v;
+    m_t[i] = m;
+    float xc = xv;
+    if (k.corr) {
+      xc = k.cx * x_last[i] + k.cs * m_s[i] + k.ct * m;
+      if (m_p) xc += k.cp * m_p[i];
+    }
+    x_last[i] = xc;
+    float xn = k.px * xc + k.pt * m;
+    if (m_s) xn += k.pp * m_s[i];
+    x[i] = xn;
+  }
+}
+
 template <typename T>
 __global__ void cast_kernel(const float* __restrict__ x, T* __restrict__ out, int64_t n) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
@@ -459,6 +486,14 @@ template <typename T>
 hipError_t launch_add(const T* a, const T* b, T* out, int64_t n, float sign, hipStream_t s) {
   if (n % Chunk<T>::E) return hipErrorInvalidValue;
   hipLaunchKernelGGL(add_kernel<T>, dim3(grid_for(n / Chunk<T>::E, 256)), dim3(256), 0, s, a, b, out, n, sign);
+  return hipGetLastError();
+}
+
+hipError_t launch_unipc(float* x, const float* v_c, const float* v_u, float g, float sig_t, float* x_last,
+                        const float* m_s, const float* m_p, float* m_t, const UniCoef& k, int64_t n,
+                        hipStream_t s) {
+  hipLaunchKernelGGL(unipc_kernel, dim3(grid_for(n, 256)), dim3(256), 0, s, x, v_c, v_u, g, sig_t, x_last, m_s,
+                     m_p, m_t, k, n);
   return hipGetLastError();
 }
 

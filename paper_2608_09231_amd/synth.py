@@ -78,6 +78,7 @@ class Workload:
     gate_widths: tuple = (8, 32, 16, 1)
     gate_std: float = 0.3
     note: str = ""
+    solver: str = "euler"   # step rule: "euler", or "unipc" (the paper's Wan sampler)
 
 
 def _m(**kw) -> ModelConfig:
@@ -120,7 +121,7 @@ WORKLOADS = {
            hidden=5120, heads=40, head_dim=128, mlp_hidden=13824,
            in_channels=64, ctx_dim=4096, n_img=32760, n_txt=512,
            pooled_text=False),
-        T=50, B=12, shift=5.0, guidance=1.0, seed=42),
+        T=50, B=12, shift=5.0, guidance=1.0, seed=42, solver="unipc"),
     # Small parity workloads: several GEMM / attention tiles and ragged tails,
     # still quick for the oracle.
     "small_bf16": Workload(

@@ -115,7 +115,7 @@ def test_full_depth_properties(name):
     h = binding.DitCache(cfg, weights.blob)
     lat = dev(torch, x0)
     txt = dev(torch, text)
-    s1 = h.sample(lat, txt, gate, w.T, w.B, shift=w.shift, guidance=w.guidance)
+    s1 = h.sample(lat, txt, gate, w.T, w.B, shift=w.shift, guidance=w.guidance, solver=w.solver)
     torch.cuda.synchronize()
     x_a = lat.cpu().numpy()
     say(f"{name}: sample 1 {time.time() - t0:.1f} s schedule {''.join(map(str, s1.full.tolist()))}")
@@ -123,11 +123,13 @@ def test_full_depth_properties(name):
     assert np.all(np.isfinite(x_a))
     # replay of its own schedule is bitwise identical
     lat.copy_(dev(torch, x0))
-    s2 = h.sample(lat, txt, gate, w.T, w.B, shift=w.shift, guidance=w.guidance, forced_mask=s1.full)
+    s2 = h.sample(lat, txt, gate, w.T, w.B, shift=w.shift, guidance=w.guidance, forced_mask=s1.full,
+                  solver=w.solver)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(lat.cpu().numpy(), x_a)
     np.testing.assert_array_equal(s2.sums[1:], s1.sums[1:])
-    # step-1 indicator sums: rerun one step on the device to get x_1
+    # step-1 indicator sums: rerun one step on the device to get x_1 (the first
+    # UniPC step is order 1 with nothing to correct, i.e. the Euler step)
     lat.copy_(dev(torch, x0))
     one = h.sample(lat, txt, gate, 1, 1, sigmas=sigma_schedule(w.T, w.shift)[:2].copy(), guidance=w.guidance)
     torch.cuda.synchronize()

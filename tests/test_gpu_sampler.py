@@ -20,7 +20,8 @@ TOL = {"f32": 1e-5, "bf16": 2e-2}
 SUM_TOL = {"f32": 1e-5, "bf16": 1e-3}
 
 
-def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5, gate=None, policy="gate", delta=0.0):
+def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5, gate=None, policy="gate", delta=0.0,
+           solver="euler"):
     torch = torch_cuda()
     w = synth.workload(name)
     cfg = w.model
@@ -28,7 +29,7 @@ def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5, gate=None, p
     gate = wgate if gate is None else gate
     T = T or w.T
     B = B or w.B
-    pol = dict(policy=policy, delta=delta)
+    pol = dict(policy=policy, delta=delta, solver=solver)
     x_gpu, sched, h = run_sampler(torch, w, weights, x0, text, gate, T=T, B=B, indicator=indicator, tau=tau,
                                   **pol)
     h.close()
@@ -43,8 +44,14 @@ def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5, gate=None, p
         check_schedule_against_oracle(sched, ores)
     err = rel_l2(x_gpu, ores.x)
     assert err <= TOL[cfg.dtype], err
-    ok = np.isfinite(ores.sums[1:])
-    np.testing.assert_allclose(sched.sums[1:][ok], ores.sums[1:][ok], rtol=SUM_TOL[cfg.dtype])
+    # magnitude sums (|m_prev|, |m_last|) to SUM_TOL relative; the difference
+    # sums carry the storage rounding of both tensors, so their error is bounded
+    # relative to the magnitude sum of the same step, not to the difference
+    got, ref = sched.sums[1:], ores.sums[1:]
+    ok = np.all(np.isfinite(ref), axis=1)
+    np.testing.assert_allclose(got[ok][:, [1, 3]], ref[ok][:, [1, 3]], rtol=SUM_TOL[cfg.dtype])
+    for d, mcol in ((0, 1), (2, 3)):
+        assert np.all(np.abs(got[ok][:, d] - ref[ok][:, d]) <= SUM_TOL[cfg.dtype] * ref[ok][:, mcol]), (d, got, ref)
     np.testing.assert_allclose(sched.features[1:, :4], ores.features[1:, :4], rtol=1e-12)
     np.testing.assert_allclose(sched.features[1:, 4:], ores.features[1:, 4:], rtol=10 * SUM_TOL[cfg.dtype])
     gated = oracle_sample(cfg, weights.tensors, gate, x0, text, T, B, shift=w.shift, tau=tau,
@@ -118,6 +125,13 @@ def test_static_policy():
 def test_threshold_policy(name, delta):
     sched, ores, _ = parity(name, policy="threshold", delta=delta, gate=np.zeros(0, np.float32))
     print(name, "threshold", delta, "nfe", sched.nfe, "schedule", sched.full.tolist())
+
+
+@pytest.mark.parametrize("name", ["tiny", "small_bf16", "small_cfg_bf16", "small_cross_bf16"])
+def test_unipc_solver(name):
+    """UniPC-2 predictor-corrector (the Wan sampler) in place of Euler."""
+    sched, ores, err = parity(name, solver="unipc")
+    print(name, "unipc rel-L2", err, "schedule", sched.full.tolist())
 
 
 def test_forced_replay_and_determinism():
