@@ -40,6 +40,15 @@ __host__ __device__ constexpr int vt_slot(int k) { return 8 * ((k >> 2) & 1) + 4
 __device__ __forceinline__ int k_off(int row, int c) { return row * 256 + ((c ^ (row & 15)) << 4); }
 __device__ __forceinline__ int v_off(int d, int c) { return d * 128 + ((c ^ ((d >> 1) & 7)) << 4); }
 
+// Rows of one joint sequence that lies in two pieces (the text rows of a
+// branch, then its image rows further down a branch-batched buffer): row r
+// is stored at r + gap once r >= split.  split = INT_MAX: one piece.
+struct RowMap {
+  int split;
+  int64_t gap;
+  __device__ __forceinline__ int64_t operator()(int r) const { return r + (r >= split ? gap : 0); }
+};
+
 constexpr int NSTAGE = 3;     // K / V^T tiles resident: t (V), t + 1 (K), t + 2 (in flight)
 constexpr int TILE_BYTES = 2 * KT * D * 2;
 
@@ -55,7 +64,7 @@ template <bool BOUNDED, int QG, int NW>
 __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
     const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restrict__ k, int64_t ldk,
     const bf16_t* __restrict__ vt, int ldvt, bf16_t* __restrict__ o, int64_t ldo, int Lq, int Lk,
-    float scale_log2) {
+    float scale_log2, RowMap rm) {
   __shared__ __attribute__((aligned(1024))) char smem[NSTAGE][TILE_BYTES];  // [stage][K | V^T]
 
   constexpr int QW = 32 * QG, QB = NW * QW;
@@ -70,7 +79,7 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
 #pragma unroll
   for (int g = 0; g < QG; ++g) {
     const int qr = min(q0 + 32 * g + lrow, Lq - 1);
-    const bf16_t* qp = q + (int64_t)qr * ldq + h * D + 8 * lhalf;
+    const bf16_t* qp = q + rm(qr) * ldq + h * D + 8 * lhalf;
 #pragma unroll
     for (int s = 0; s < 8; ++s) qf[g][s] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(qp + 16 * s));
   }
@@ -90,7 +99,7 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
         const int row = 4 * ii + (lane >> 4);
         const int c = (lane & 15) ^ (row & 15);
         const int key = min(kb0 + row, Lk - 1);
-        __builtin_amdgcn_global_load_lds((glb_void_t*)(kh + (int64_t)key * ldk + c * 8),
+        __builtin_amdgcn_global_load_lds((glb_void_t*)(kh + rm(key) * ldk + c * 8),
                                          (lds_void_t*)(sk + ii * 1024), 16, 0, 0);
       }
       {  // V^T rows 8 ii .. 8 ii + 7
@@ -226,7 +235,7 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
     const float l = l_run[g] + __shfl_xor(l_run[g], 32, 64);
     const float inv = 1.f / l;
     if (qi < Lq) {
-      bf16_t* op = o + (int64_t)qi * ldo + h * D;
+      bf16_t* op = o + rm(qi) * ldo + h * D;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -241,14 +250,14 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
 
 // vt[h][d][16 g + vt_slot(k)] = v[16 g + k][h*128 + d] for keys < Lk, 0 up to ldvt.
 __global__ __launch_bounds__(256) void transpose_v_kernel(const bf16_t* __restrict__ v, int64_t ldv,
-                                                          bf16_t* __restrict__ vt, int Lk, int ldvt) {
+                                                          bf16_t* __restrict__ vt, int Lk, int ldvt, RowMap rm) {
   __shared__ bf16_t tile[64][D + 2];
   const int l0 = blockIdx.x * 64, h = blockIdx.y, tid = threadIdx.x;
   for (int i = tid; i < 64 * (D / 2); i += 256) {
     const int r = i / (D / 2), c2 = i % (D / 2);
     const int l = l0 + r;
     uint32_t w = 0;
-    if (l < Lk) w = *(const uint32_t*)(v + (int64_t)l * ldv + h * D + 2 * c2);
+    if (l < Lk) w = *(const uint32_t*)(v + rm(l) * ldv + h * D + 2 * c2);
     const int rs = (r & ~15) | vt_slot(r & 15);
     tile[rs][2 * c2] = (bf16_t)(w & 0xffff);
     tile[rs][2 * c2 + 1] = (bf16_t)(w >> 16);
@@ -312,16 +321,16 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 }  // namespace
 
 hipError_t launch_transpose_v_bf16(const void* v, int64_t ldv, void* vt, int Lk, int heads,
-                                   hipStream_t s) {
+                                   hipStream_t s, int split, int64_t gap) {
   const int ldvt = (Lk + 63) / 64 * 64;
   hipLaunchKernelGGL(transpose_v_kernel, dim3(ldvt / 64, heads), dim3(256), 0, s,
-                     (const bf16_t*)v, ldv, (bf16_t*)vt, Lk, ldvt);
+                     (const bf16_t*)v, ldv, (bf16_t*)vt, Lk, ldvt, RowMap{split, gap});
   return hipGetLastError();
 }
 
 hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int64_t ldk,
                                   const void* vt, int ldvt, void* o, int64_t ldo, int Lq, int Lk,
-                                  int heads, bool bounded_logits, hipStream_t s) {
+                                  int heads, bool bounded_logits, hipStream_t s, int split, int64_t gap) {
   // 32 queries per wave, 8 waves: about 190 registers per lane, so two
   // waves share each SIMD and one wave's softmax overlaps the other's MFMAs.
   constexpr int kQG = 1, kNW = 8;
@@ -331,11 +340,11 @@ hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int
   if (bounded_logits)
     hipLaunchKernelGGL((flash_attn_bf16_kernel<true, kQG, kNW>), grid, dim3(64 * kNW), 0, s,
                        (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o,
-                       ldo, Lq, Lk, scale_log2);
+                       ldo, Lq, Lk, scale_log2, RowMap{split, gap});
   else
     hipLaunchKernelGGL((flash_attn_bf16_kernel<false, kQG, kNW>), grid, dim3(64 * kNW), 0, s,
                        (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o,
-                       ldo, Lq, Lk, scale_log2);
+                       ldo, Lq, Lk, scale_log2, RowMap{split, gap});
   return hipGetLastError();
 }
 

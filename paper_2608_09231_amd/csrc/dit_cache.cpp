@@ -76,6 +76,10 @@ struct dit_cache {
   bool bf16 = true;
   size_t esz = 2;
   int H = 0, F = 0, N = 0, Nt = 0, L = 0, C = 0, nb = 1, n_mod = 0, ldY = 0;
+  // guidance pair whose branches share every modulation vector (no pooled
+  // text): both branches run the block stack together, stream-major rows
+  // [txt_0; txt_1; img_0; img_1] (see full_stack_pair)
+  bool pair_batched = false;
 
   void* wdev = nullptr;
   size_t wbytes = 0;
@@ -247,18 +251,19 @@ dit_status ln_mod(dit_cache* c, const void* x, int64_t ldx, void* out, int64_t l
 
 // attention over joint rows: q,k,v inside Y (or separate), output into o
 dit_status attention(dit_cache* c, const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v,
-                     int64_t ldv, void* o, int64_t ldo, int Lq, int Lk, void* vt_ws) {
+                     int64_t ldv, void* o, int64_t ldo, int Lq, int Lk, void* vt_ws, int split = 0x7fffffff,
+                     int64_t gap = 0) {
   const int heads = c->cfg.heads, hd = c->cfg.head_dim;
   const double flops = 4.0 * Lq * (double)Lk * heads * hd;
   if (c->bf16) {
     {
       Scope s(c, DIT_K_FULL_OTHER, 2.0 * Lk * heads * hd * 2);
-      HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt_ws, Lk, heads, c->stream));
+      HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt_ws, Lk, heads, c->stream, split, gap));
     }
     Scope s(c, DIT_K_ATTN, flops);
     // q and k leave the projection through a unit-gain RMS norm: bounded logits
     HIPCK(dit::launch_flash_attn_bf16(q, ldq, k, ldk, vt_ws, (int)rup(Lk, 64), o, ldo, Lq, Lk, heads,
-                                      true, c->stream));
+                                      true, c->stream, split, gap));
   } else {
     Scope s(c, DIT_K_ATTN, flops);
     HIPCK(dit::launch_attn_f32((const float*)q, ldq, (const float*)k, ldk, (const float*)v, ldv,
@@ -358,9 +363,10 @@ dit_status alloc_workspace(dit_cache* c) {
   TRY(dalloc(c, &c->h, (size_t)N * H * e));
   for (auto& m : c->mbuf) TRY(dalloc(c, &m, (size_t)N * H * e));
   TRY(dalloc(c, &c->r, (size_t)c->nb * N * H * e));
-  TRY(dalloc(c, &c->X, (size_t)L * H * e));
-  TRY(dalloc(c, &c->A, (size_t)L * H * e));
-  TRY(dalloc(c, &c->Y, (size_t)L * c->ldY * e));
+  const size_t LB = (size_t)L * (c->pair_batched ? c->nb : 1);  // block-stack rows
+  TRY(dalloc(c, &c->X, LB * H * e));
+  TRY(dalloc(c, &c->A, LB * H * e));
+  TRY(dalloc(c, &c->Y, LB * c->ldY * e));
   if (c->bf16) TRY(dalloc(c, &c->vt, (size_t)c->cfg.heads * 128 * rup(L, 64) * 2));
   TRY(dalloc(c, &c->yf, (size_t)N * H * e));
   TRY(dalloc(c, &c->vel, (size_t)c->nb * N * c->C * 4));
@@ -639,6 +645,82 @@ dit_status full_stack(dit_cache* c, int b, const StepCtx& s) {
     }));
   }
   (void)F;
+  return DIT_OK;
+}
+
+// Both branches of a guidance pair through the MMDiT stack at once (bf16, one
+// modulation table for both).  Rows are stream-major, [txt_0; txt_1; img_0;
+// img_1], so each linear layer is one launch over both branches' rows of a
+// stream (twice the rows per weight read); attention runs per branch on its
+// two row pieces (text rows, then image rows nb Nt + b N rows down).
+dit_status full_stack_pair(dit_cache* c, const StepCtx& s) {
+  const int H = c->H, N = c->N, Nt = c->Nt, L = c->L, ldY = c->ldY, nb = c->nb;
+  const int Lt = nb * Nt, Li = nb * N, LL = nb * L;
+  const float* md = s.modp[0];
+  char* Xi = sp(c, c->X, (size_t)Lt * H);
+  char* Ai = sp(c, c->A, (size_t)Lt * H);
+  char* Yi = sp(c, c->Y, (size_t)Lt * ldY);
+  const int cls = DIT_K_GEMM;
+  for (int b = 0; b < nb; ++b) {
+    HIPCK(hipMemcpyAsync(sp(c, c->X, (size_t)b * Nt * H), sp(c, c->txt, (size_t)b * Nt * H),
+                         (size_t)Nt * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
+    HIPCK(hipMemcpyAsync(sp(c, Xi, (size_t)b * N * H), c->h, (size_t)N * H * c->esz, hipMemcpyDeviceToDevice,
+                         c->stream));
+  }
+  // branch b's joint sequence: text rows from row b Nt, image rows from row Lt + b N
+  auto attn_b = [&](int b) {
+    const char* y0 = sp(c, c->Y, (size_t)b * Nt * ldY);
+    const int64_t gap = (int64_t)(nb - 1 - b) * Nt + (int64_t)b * N;
+    return attention(c, y0, ldY, y0 + (size_t)H * c->esz, ldY, y0 + (size_t)2 * H * c->esz, ldY,
+                     (void*)(y0 + (size_t)3 * H * c->esz), ldY, L, L, c->vt, Nt, gap);
+  };
+  for (int i = 0; i < c->cfg.n_double; ++i) {
+    const DoubleW& w = c->M.dbl[i];
+    const float* mi = md + (size_t)12 * H * i;
+    const float* mt = mi + 6 * H;
+    TRY(ln_mod(c, c->X, H, c->A, H, LL, Lt, mt, mt + H, mi, mi + H, DIT_K_FULL_OTHER));
+    GemmArgs g[2];
+    g[0] = lin_args(c, Ai, H, w.qkv[0], Yi, ldY, Li);
+    g[1] = lin_args(c, c->A, H, w.qkv[1], c->Y, ldY, Lt);
+    g[0].rms_cols = g[1].rms_cols = 2 * H;
+    TRY(gemm(c, g, 2, cls));
+    for (int b = 0; b < nb; ++b) TRY(attn_b(b));
+    g[0] = lin_args(c, Yi + 3 * H * c->esz, ldY, w.o[0], Xi, H, Li, DIT_EPI_GATED_RES);
+    g[1] = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.o[1], c->X, H, Lt, DIT_EPI_GATED_RES);
+    g[0].gate = mi + 2 * H;
+    g[1].gate = mt + 2 * H;
+    TRY(gemm(c, g, 2, cls));
+    TRY(ln_mod(c, c->X, H, c->A, H, LL, Lt, mt + 3 * H, mt + 4 * H, mi + 3 * H, mi + 4 * H, DIT_K_FULL_OTHER));
+    g[0] = lin_args(c, Ai, H, w.mlp0[0], Yi + 4 * H * c->esz, ldY, Li);
+    g[1] = lin_args(c, c->A, H, w.mlp0[1], sp(c, c->Y, 4 * H), ldY, Lt);
+    g[0].gelu_from = g[1].gelu_from = 0;
+    TRY(gemm(c, g, 2, cls));
+    g[0] = lin_args(c, Yi + 4 * H * c->esz, ldY, w.mlp1[0], Xi, H, Li, DIT_EPI_GATED_RES);
+    g[1] = lin_args(c, sp(c, c->Y, 4 * H), ldY, w.mlp1[1], c->X, H, Lt, DIT_EPI_GATED_RES);
+    g[0].gate = mi + 5 * H;
+    g[1].gate = mt + 5 * H;
+    TRY(gemm(c, g, 2, cls));
+  }
+  for (int i = 0; i < c->cfg.n_single; ++i) {
+    const SingleW& w = c->M.sgl[i];
+    const float* ms = md + (size_t)12 * H * c->cfg.n_double + (size_t)3 * H * i;
+    TRY(ln_mod(c, c->X, H, c->A, H, LL, LL, ms, ms + H, ms, ms + H, DIT_K_FULL_OTHER));
+    GemmArgs g = lin_args(c, c->A, H, w.l1, c->Y, ldY, LL);
+    g.rms_cols = 2 * H;
+    g.gelu_from = 3 * H;
+    g.gap_at = 3 * H;
+    g.gap = H;
+    TRY(gemm(c, &g, 1, cls));
+    for (int b = 0; b < nb; ++b) TRY(attn_b(b));
+    g = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.l2, c->X, H, LL, DIT_EPI_GATED_RES);
+    g.gate = ms + 2 * H;
+    TRY(gemm(c, &g, 1, cls));
+  }
+  for (int b = 0; b < nb; ++b) {
+    Scope sc(c, DIT_K_FULL_OTHER, 3.0 * N * H * c->esz);
+    HIPCK(dit::launch_add<bf16_t>((const bf16_t*)sp(c, Xi, (size_t)b * N * H), (const bf16_t*)c->h,
+                                  (bf16_t*)sp(c, c->r, (size_t)b * N * H), (int64_t)N * H, -1.f, c->stream));
+  }
   return DIT_OK;
 }
 
@@ -949,10 +1031,16 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
       }
       const bool fused_euler = !pair && proj_fits(c) && !unipc;
       float* lat_f = fused_euler ? latent : nullptr;
+      if (dec && c->pair_batched) TRY(full_stack_pair(c, s));
       for (int b = 0; b < c->nb; ++b) {
         if (dec) {
-          TRY(full_stack(c, b, s));
-          const void* hout = c->cfg.n_cross ? c->X : sp(c, c->X, (size_t)c->Nt * H);
+          const void* hout;
+          if (c->pair_batched) {
+            hout = sp(c, c->X, (size_t)c->nb * c->Nt * H + (size_t)b * N * H);
+          } else {
+            TRY(full_stack(c, b, s));
+            hout = c->cfg.n_cross ? c->X : sp(c, c->X, (size_t)c->Nt * H);
+          }
           TRY(final_layer(c, b, hout, s, DIT_K_FULL_OTHER, lat_f, dsig));
         } else {
           {
@@ -1027,6 +1115,7 @@ dit_status dit_cache_create(const dit_model_config* cfg, const void* weights, si
   c->H = cfg->hidden; c->F = cfg->mlp_hidden; c->N = cfg->n_img; c->Nt = cfg->n_txt;
   c->L = cfg->n_cross ? cfg->n_img : cfg->n_img + cfg->n_txt;
   c->C = cfg->in_channels; c->nb = cfg->batch;
+  c->pair_batched = c->bf16 && c->nb == 2 && !cfg->pooled_text && !cfg->n_cross;
   c->n_mod = 12 * c->H * cfg->n_double + 3 * c->H * cfg->n_single + (cfg->n_cross ? 6 * c->H : 0) + 2 * c->H;
   c->ldY = 4 * c->H + c->F;
   int dev = 0;

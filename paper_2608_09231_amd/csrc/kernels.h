@@ -33,12 +33,15 @@ hipError_t launch_proj_small_n(const void* A, int64_t lda, const void* W, int64_
 hipError_t launch_gemm_f32(const GemmArgs* g, int n, hipStream_t s);
 
 // Flash attention, bf16, head_dim 128. vt = v transposed per head:
-// [heads][128][ldvt], ldvt = round_up(Lk, 64), zero padded.
+// [heads][128][ldvt], ldvt = round_up(Lk, 64), zero padded.  Rows r >= split
+// of q, k, v and o are stored gap rows further down (a joint sequence split
+// over a branch-batched buffer); split = INT_MAX for one contiguous piece.
 hipError_t launch_transpose_v_bf16(const void* v, int64_t ldv, void* vt, int Lk, int heads,
-                                   hipStream_t s);
+                                   hipStream_t s, int split = 0x7fffffff, int64_t gap = 0);
 hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int64_t ldk,
                                   const void* vt, int ldvt, void* o, int64_t ldo, int Lq,
-                                  int Lk, int heads, bool bounded_logits, hipStream_t s);
+                                  int Lk, int heads, bool bounded_logits, hipStream_t s,
+                                  int split = 0x7fffffff, int64_t gap = 0);
 // f32 attention, head_dim <= 128 (multiple of 4).
 hipError_t launch_attn_f32(const float* q, int64_t ldq, const float* k, int64_t ldk,
                            const float* v, int64_t ldv, float* o, int64_t ldo, int Lq, int Lk,
