@@ -126,6 +126,55 @@ def gemm_traffic(workload):
     return data["traffic_bytes_per_launch"]
 
 
+def multi_prompt(h, w, lat0, args, ms_single):
+    """P prompts (own latents and texts) through dit_cache_sample_batch: each
+    keeps its own schedule, the computing ones share the block-stack
+    launches.  Timed like the single-sample leg (same step and warmup
+    counts, inputs resident)."""
+    import torch
+
+    from paper_2608_09231_amd import synth
+    cfg = w.model
+    P = args.prompts
+    xs = np.stack([synth.make_latent(cfg, w.seed + 101 * j) for j in range(P)])
+    ts = np.stack([synth.make_text(cfg, w.seed + 211 * j + 1) for j in range(P)])
+    gate = synth.make_gate_blob(w.gate_widths, w.seed, w.gate_std)
+    lats0 = torch.from_numpy(xs).cuda()
+    txts = torch.from_numpy(ts.view(np.int16) if ts.dtype == np.uint16 else ts).cuda()
+    lats = lats0.clone()
+
+    def one():
+        lats.copy_(lats0)
+        return h.sample_batch(lats, txts, gate, w.T, w.B, shift=w.shift, guidance=w.guidance, solver=w.solver)
+
+    for _ in range(args.warmup):
+        one()
+    torch.cuda.synchronize()
+    h.reset_stats()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        scheds = one()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    st = h.stats()
+    full = np.stack([s.full for s in scheds])
+    per_step = full.sum(axis=0)
+    log(f"[bench] multi-prompt: {args.steps} x {P} samples in {dt:.3f} s; computing samples per step "
+        f"{''.join(map(str, per_step.tolist()))}")
+    ms_batch = dt / args.steps * 1e3
+    return {
+        "prompts": P,
+        "samples_per_s": P / (ms_batch * 1e-3),
+        "steps_per_s": P * w.T / (ms_batch * 1e-3),
+        "ms_per_batch": ms_batch,
+        "speedup_vs_one_at_a_time": P * ms_single / ms_batch,
+        "stacked_steps": int((per_step > 0).sum()),
+        "mean_samples_per_stacked_step": float(per_step[per_step > 0].mean()),
+        "host_gate_ms_per_batch": st["host_gate_ms"] / max(args.steps, 1),
+        "data": "prompt j: latent seed + 101 j, text seed + 211 j + 1; one gate for all",
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -134,6 +183,8 @@ def main():
     ap.add_argument("--workload", default="flux1024")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
+    ap.add_argument("--prompts", type=int, default=4,
+                    help="multi-prompt leg: this many prompts sampled together (0 or 1: skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 256 MiB device-to-device copy first (HBM counter calibration)")
     args = ap.parse_args()
@@ -247,6 +298,8 @@ def main():
         },
         "paper_context": "paper: FLUX.1-dev 1024^2, T=50, 31.13 s full compute, BAG B=9 5.99 s on one RTX 4090 (Tab. 1); not comparable hardware or T",
     }
+    if args.prompts > 1:
+        out["multi_prompt"] = multi_prompt(h, w, lat0, args, ms_per_sample)
     h.close()
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define DIT_ABI_VERSION 3
+#define DIT_ABI_VERSION 4
 #define DIT_N_FEATURES 8
 
 typedef enum dit_status {
@@ -176,6 +176,29 @@ dit_status dit_cache_sample(dit_cache* h, float* latent, const void* text_emb, i
 dit_status dit_cache_sample_ex(dit_cache* h, float* latent, const void* text_emb,
                                const float* gate_weights, size_t gate_len,
                                const dit_sample_params* p, dit_schedule* out);
+
+/* n_samples independent samples (one prompt each) advanced in lockstep, each
+ * with its own schedule (Sec. 3.1 poses the problem per prompt p): at
+ * every step the library forms and reduces every sample's indicator, waits
+ * once for all their sums, decides per sample (Alg. 2 with that sample's
+ * own budget state), reuses the cached residuals of the samples that skip,
+ * and runs the block stack of the samples that compute together: every
+ * linear layer is one GEMM launch over all their rows, attention one launch
+ * over all their sequences.  Sample j's result is the result of
+ * dit_cache_sample_ex on its own inputs, up to the rounding of the stacked
+ * launches.
+ *   latents   device, f32 [n_samples, n_img, in_channels]: x_0 in, x_T out
+ *   text_emb  device, storage dtype [n_samples, batch, n_txt, ctx_dim]
+ *   p         shared by all samples; p->forced_mask, if not NULL, is host
+ *             [n_samples, T] (one replay mask per sample)
+ *   out       host array of n_samples schedules, one per sample
+ * Workspace for n_samples is allocated on first use and kept (per sample
+ * about 6 [n_img, hidden] tensors plus, for the stacked block stack, the
+ * rows of every sequence).  On error every latent is unspecified and each
+ * out[j].steps_done holds the steps that sample completed. */
+dit_status dit_cache_sample_batch(dit_cache* h, int32_t n_samples, float* latents, const void* text_emb,
+                                  const float* gate_weights, size_t gate_len,
+                                  const dit_sample_params* p, dit_schedule* out);
 
 void dit_cache_destroy(dit_cache* h);
 

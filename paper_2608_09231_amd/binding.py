@@ -22,14 +22,15 @@ STATUS_NAMES = {0: "DIT_OK", -1: "DIT_EINVAL", -2: "DIT_ENOMEM", -3: "DIT_EHIP",
 DTYPE_F32, DTYPE_BF16 = 0, 1
 INDICATOR_MODULATED, INDICATOR_PATCH = 0, 1
 EPI_STORE, EPI_F32, EPI_GATED_RES, EPI_SILU = 0, 1, 2, 4
-ABI_VERSION = 3
+ABI_VERSION = 4
 POLICIES = {"gate": 0, "static": 1, "threshold": 2}
 SOLVERS = {"euler": 0, "unipc": 1}
 N_FEATURES = 8
 K_CLASSES = ["gemm", "attn", "indicator", "reuse", "full_other", "once"]
 
 # Every symbol the headers declare.
-EXPORTS = ["dit_cache_create", "dit_cache_sample", "dit_cache_sample_ex", "dit_cache_destroy",
+EXPORTS = ["dit_cache_create", "dit_cache_sample", "dit_cache_sample_ex", "dit_cache_sample_batch",
+           "dit_cache_destroy",
            "dit_cache_last_error", "dit_cache_set_profiling", "dit_cache_get_stats",
            "dit_cache_reset_stats", "dit_gemm_bf16", "dit_attention_bf16"]
 
@@ -89,6 +90,8 @@ def load(path: str = LIB_PATH):
     lib.dit_cache_create.argtypes = [C.POINTER(ModelConfigC), vp, sz, vp, C.POINTER(vp)]
     lib.dit_cache_sample.argtypes = [vp, vp, vp, C.c_int32, C.c_int32, vp, sz, C.POINTER(ScheduleC)]
     lib.dit_cache_sample_ex.argtypes = [vp, vp, vp, vp, sz, C.POINTER(SampleParamsC), C.POINTER(ScheduleC)]
+    lib.dit_cache_sample_batch.argtypes = [vp, C.c_int32, vp, vp, vp, sz, C.POINTER(SampleParamsC),
+                                           C.POINTER(ScheduleC)]
     lib.dit_cache_destroy.argtypes = [vp]
     lib.dit_cache_destroy.restype = None
     lib.dit_cache_last_error.argtypes = [vp]
@@ -164,6 +167,42 @@ class DitCache:
         except Exception:
             pass
 
+    @staticmethod
+    def _params(T, B, sigmas, shift, tau, guidance, forced_mask, indicator, policy, delta, solver):
+        sig = None if sigmas is None else np.ascontiguousarray(sigmas, np.float64)
+        fm = None if forced_mask is None else np.ascontiguousarray(forced_mask, np.uint8)
+        p = SampleParamsC(int(T), int(B),
+                          sig.ctypes.data_as(C.POINTER(C.c_double)) if sig is not None else None,
+                          float(shift), float(tau), float(guidance),
+                          fm.ctypes.data_as(C.POINTER(C.c_uint8)) if fm is not None else None,
+                          INDICATOR_PATCH if indicator == "patch" else INDICATOR_MODULATED,
+                          POLICIES[policy], float(delta), SOLVERS[solver])
+        return p, (sig, fm)  # the arrays stay alive with the struct
+
+    @staticmethod
+    def _schedules(S, T):
+        arrs = [(np.zeros(T, np.uint8), np.zeros(T, np.float32), np.zeros(T, np.uint8),
+                 np.zeros(T * N_FEATURES, np.float64), np.zeros(T * 4, np.float64)) for _ in range(S)]
+        cs = (ScheduleC * S)()
+        for j, (full, logit, forced, feats, sums) in enumerate(arrs):
+            cs[j] = ScheduleC(full.ctypes.data_as(C.POINTER(C.c_uint8)),
+                              logit.ctypes.data_as(C.POINTER(C.c_float)),
+                              forced.ctypes.data_as(C.POINTER(C.c_uint8)),
+                              feats.ctypes.data_as(C.POINTER(C.c_double)),
+                              sums.ctypes.data_as(C.POINTER(C.c_double)), 0, 0)
+        return arrs, cs
+
+    @staticmethod
+    def _results(arrs, cs, T):
+        return [Schedule(full, logit, forced, feats.reshape(T, N_FEATURES), sums.reshape(T, 4),
+                         cs[j].nfe, cs[j].steps_done)
+                for j, (full, logit, forced, feats, sums) in enumerate(arrs)]
+
+    def _raise(self, st, res):
+        err = DitError(st, _lib.dit_cache_last_error(self._h).decode())
+        err.schedule = res
+        raise err
+
     def sample(self, latent, text_emb, gate_blob, T, B, *, sigmas=None, shift=1.0, tau=0.5,
                guidance=1.0, forced_mask=None, indicator="modulated", policy="gate",
                delta=0.0, solver="euler") -> Schedule:
@@ -173,35 +212,39 @@ class DitCache:
         latter two do not read gate_blob, which may be None); solver
         "euler" | "unipc"."""
         gate = np.ascontiguousarray(gate_blob if gate_blob is not None else [], np.float32)
-        full = np.zeros(T, np.uint8)
-        logit = np.zeros(T, np.float32)
-        forced = np.zeros(T, np.uint8)
-        feats = np.zeros(T * N_FEATURES, np.float64)
-        sums = np.zeros(T * 4, np.float64)
-        sched = ScheduleC(full.ctypes.data_as(C.POINTER(C.c_uint8)),
-                          logit.ctypes.data_as(C.POINTER(C.c_float)),
-                          forced.ctypes.data_as(C.POINTER(C.c_uint8)),
-                          feats.ctypes.data_as(C.POINTER(C.c_double)),
-                          sums.ctypes.data_as(C.POINTER(C.c_double)), 0, 0)
-        sig = None if sigmas is None else np.ascontiguousarray(sigmas, np.float64)
-        fm = None if forced_mask is None else np.ascontiguousarray(forced_mask, np.uint8)
-        p = SampleParamsC(int(T), int(B),
-                          sig.ctypes.data_as(C.POINTER(C.c_double)) if sig is not None else None,
-                          float(shift), float(tau), float(guidance),
-                          fm.ctypes.data_as(C.POINTER(C.c_uint8)) if fm is not None else None,
-                          INDICATOR_PATCH if indicator == "patch" else INDICATOR_MODULATED,
-                          POLICIES[policy], float(delta), SOLVERS[solver])
+        arrs, cs = self._schedules(1, T)
+        p, keep = self._params(T, B, sigmas, shift, tau, guidance, forced_mask, indicator, policy, delta, solver)
         st = _lib.dit_cache_sample_ex(self._h, C.c_void_p(latent.data_ptr()),
                                       C.c_void_p(text_emb.data_ptr()),
                                       gate.ctypes.data_as(C.c_void_p) if gate.size else None, gate.size,
-                                      C.byref(p),
-                                      C.byref(sched))
-        res = Schedule(full, logit, forced, feats.reshape(T, N_FEATURES), sums.reshape(T, 4),
-                       sched.nfe, sched.steps_done)
+                                      C.byref(p), cs)
+        res = self._results(arrs, cs, T)[0]
         if st != DIT_OK:
-            err = DitError(st, _lib.dit_cache_last_error(self._h).decode())
-            err.schedule = res
-            raise err
+            self._raise(st, res)
+        return res
+
+    def sample_batch(self, latents, text_embs, gate_blob, T, B, *, sigmas=None, shift=1.0, tau=0.5,
+                     guidance=1.0, forced_masks=None, indicator="modulated", policy="gate",
+                     delta=0.0, solver="euler") -> list:
+        """dit_cache_sample_batch: latents torch f32 cuda [S, N, C] (in
+        place), text_embs [S, batch, N_t, ctx] in the storage dtype,
+        forced_masks None or [S, T]; one Schedule per sample."""
+        S = int(latents.shape[0])
+        if S != int(text_embs.shape[0]):
+            raise ValueError("latents and text_embs disagree on the number of samples")
+        if forced_masks is not None and np.shape(forced_masks) != (S, T):
+            raise ValueError("forced_masks must be [n_samples, T]")
+        gate = np.ascontiguousarray(gate_blob if gate_blob is not None else [], np.float32)
+        arrs, cs = self._schedules(S, T)
+        p, keep = self._params(T, B, sigmas, shift, tau, guidance, forced_masks, indicator, policy, delta,
+                               solver)
+        st = _lib.dit_cache_sample_batch(self._h, S, C.c_void_p(latents.data_ptr()),
+                                         C.c_void_p(text_embs.data_ptr()),
+                                         gate.ctypes.data_as(C.c_void_p) if gate.size else None, gate.size,
+                                         C.byref(p), cs)
+        res = self._results(arrs, cs, T)
+        if st != DIT_OK:
+            self._raise(st, res)
         return res
 
     def set_profiling(self, on: bool):

@@ -41,12 +41,20 @@ __device__ __forceinline__ int k_off(int row, int c) { return row * 256 + ((c ^ 
 __device__ __forceinline__ int v_off(int d, int c) { return d * 128 + ((c ^ ((d >> 1) & 7)) << 4); }
 
 // Rows of one joint sequence that lies in two pieces (the text rows of a
-// branch, then its image rows further down a branch-batched buffer): row r
-// is stored at r + gap once r >= split.  split = INT_MAX: one piece.
+// sequence, then its image rows further down a buffer of several stacked
+// sequences): row r is stored at base + r, plus gap once r >= split.
+// split = INT_MAX: one piece.
 struct RowMap {
   int split;
-  int64_t gap;
-  __device__ __forceinline__ int64_t operator()(int r) const { return r + (r >= split ? gap : 0); }
+  int64_t gap, base;
+  __device__ __forceinline__ int64_t operator()(int r) const { return base + r + (r >= split ? gap : 0); }
+};
+
+// Sequence z of a launch (blockIdx.z): base z * zs, gap gap0 + z * gz.
+struct SeqMap {
+  int split;
+  int64_t gap0, gz, zs;
+  __device__ __forceinline__ RowMap at(int z) const { return RowMap{split, gap0 + z * gz, z * zs}; }
 };
 
 constexpr int NSTAGE = 3;     // K / V^T tiles resident: t (V), t + 1 (K), t + 2 (in flight)
@@ -64,8 +72,10 @@ template <bool BOUNDED, int QG, int NW>
 __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
     const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restrict__ k, int64_t ldk,
     const bf16_t* __restrict__ vt, int ldvt, bf16_t* __restrict__ o, int64_t ldo, int Lq, int Lk,
-    float scale_log2, RowMap rm) {
+    float scale_log2, SeqMap sm) {
   __shared__ __attribute__((aligned(1024))) char smem[NSTAGE][TILE_BYTES];  // [stage][K | V^T]
+  const RowMap rm = sm.at(blockIdx.z);
+  vt += (int64_t)blockIdx.z * gridDim.y * D * ldvt;
 
   constexpr int QW = 32 * QG, QB = NW * QW;
   constexpr int CPW = 16 / NW;  // 1 KB copies per wave for each of K and V^T
@@ -250,8 +260,10 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
 
 // vt[h][d][16 g + vt_slot(k)] = v[16 g + k][h*128 + d] for keys < Lk, 0 up to ldvt.
 __global__ __launch_bounds__(256) void transpose_v_kernel(const bf16_t* __restrict__ v, int64_t ldv,
-                                                          bf16_t* __restrict__ vt, int Lk, int ldvt, RowMap rm) {
+                                                          bf16_t* __restrict__ vt, int Lk, int ldvt, SeqMap sm) {
   __shared__ bf16_t tile[64][D + 2];
+  const RowMap rm = sm.at(blockIdx.z);
+  vt += (int64_t)blockIdx.z * gridDim.y * D * ldvt;
   const int l0 = blockIdx.x * 64, h = blockIdx.y, tid = threadIdx.x;
   for (int i = tid; i < 64 * (D / 2); i += 256) {
     const int r = i / (D / 2), c2 = i % (D / 2);
@@ -321,30 +333,34 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 }  // namespace
 
 hipError_t launch_transpose_v_bf16(const void* v, int64_t ldv, void* vt, int Lk, int heads,
-                                   hipStream_t s, int split, int64_t gap) {
+                                   hipStream_t s, int split, int64_t gap, int nseq, int64_t zs, int64_t gz) {
+  if (nseq < 1 || Lk < 1) return hipErrorInvalidValue;
   const int ldvt = (Lk + 63) / 64 * 64;
-  hipLaunchKernelGGL(transpose_v_kernel, dim3(ldvt / 64, heads), dim3(256), 0, s,
-                     (const bf16_t*)v, ldv, (bf16_t*)vt, Lk, ldvt, RowMap{split, gap});
+  hipLaunchKernelGGL(transpose_v_kernel, dim3(ldvt / 64, heads, nseq), dim3(256), 0, s,
+                     (const bf16_t*)v, ldv, (bf16_t*)vt, Lk, ldvt, SeqMap{split, gap, gz, zs});
   return hipGetLastError();
 }
 
 hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int64_t ldk,
                                   const void* vt, int ldvt, void* o, int64_t ldo, int Lq, int Lk,
-                                  int heads, bool bounded_logits, hipStream_t s, int split, int64_t gap) {
+                                  int heads, bool bounded_logits, hipStream_t s, int split, int64_t gap,
+                                  int nseq, int64_t zs, int64_t gz) {
+  if (nseq < 1 || Lq < 1 || Lk < 1) return hipErrorInvalidValue;
   // 32 queries per wave, 8 waves: about 190 registers per lane, so two
   // waves share each SIMD and one wave's softmax overlaps the other's MFMAs.
   constexpr int kQG = 1, kNW = 8;
   constexpr int QB = 32 * kQG * kNW;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
-  const dim3 grid((Lq + QB - 1) / QB, heads);
+  const dim3 grid((Lq + QB - 1) / QB, heads, nseq);
+  const SeqMap sm{split, gap, gz, zs};
   if (bounded_logits)
     hipLaunchKernelGGL((flash_attn_bf16_kernel<true, kQG, kNW>), grid, dim3(64 * kNW), 0, s,
                        (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o,
-                       ldo, Lq, Lk, scale_log2, RowMap{split, gap});
+                       ldo, Lq, Lk, scale_log2, sm);
   else
     hipLaunchKernelGGL((flash_attn_bf16_kernel<false, kQG, kNW>), grid, dim3(64 * kNW), 0, s,
                        (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o,
-                       ldo, Lq, Lk, scale_log2, RowMap{split, gap});
+                       ldo, Lq, Lk, scale_log2, sm);
   return hipGetLastError();
 }
 

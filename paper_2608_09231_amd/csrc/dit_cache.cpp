@@ -69,6 +69,19 @@ struct Pending {
 
 }  // namespace
 
+// One sample's device state and its pacing-rule state (Alg. 2).
+struct Lane {
+  void* h = nullptr;        // [N, H] patch embedding of this step (the block stack's input)
+  void* mbuf[3] = {};       // [N, H] indicator tensors (rotating)
+  void* r = nullptr;        // [nb, N, H] cached residual per branch
+  void* txt = nullptr;      // [nb, Nt, H] projected text tokens
+  float* x_last = nullptr;  // f32 [N, C]: UniPC's corrected sample of the previous step
+  float* mh[3] = {};        // f32 [N, C]: UniPC data predictions (rotating)
+  int cnt = 0, t_last = 0, i_prev = -1, i_last = -1, i_new = 0;
+  double acc = 0.0;
+  bool dec = true;
+};
+
 struct dit_cache {
   dit_model_config cfg{};
   hipStream_t stream = nullptr;
@@ -76,42 +89,42 @@ struct dit_cache {
   bool bf16 = true;
   size_t esz = 2;
   int H = 0, F = 0, N = 0, Nt = 0, L = 0, C = 0, nb = 1, n_mod = 0, ldY = 0;
-  // guidance pair whose branches share every modulation vector (no pooled
-  // text): both branches run the block stack together, stream-major rows
-  // [txt_0; txt_1; img_0; img_1] (see full_stack_pair)
-  bool pair_batched = false;
+  // bf16 MMDiT: every sequence computed at a step (each branch of each
+  // sample that computes) runs the block stack together, stream-major rows
+  // [txt_0; ...; txt_{Q-1}; img_0; ...; img_{Q-1}] (see full_stack_multi)
+  bool stacked = false;
 
   void* wdev = nullptr;
   size_t wbytes = 0;
   Model M;
 
+  std::vector<Lane> lanes;  // per-sample state, grown on demand
+  int cap_seq = 0;          // sequences the block-stack workspace holds
+
   // workspace (storage dtype unless noted)
   void* xs = nullptr;      // [N, C]
-  void* h = nullptr;       // [N, H]
-  void* mbuf[3] = {};      // [N, H] indicator tensors (rotating)
-  void* r = nullptr;       // [nb, N, H] cached residual per branch
-  void* X = nullptr;       // [L, H] joint hidden state
-  void* A = nullptr;       // [L, H] modulated block input
-  void* Y = nullptr;       // [L, 4H+F]: q | k | v | attn out | mlp hidden
-  void* vt = nullptr;      // bf16 [heads, 128, round_up(L, 64)]
+  void* X = nullptr;       // [cap_seq L, H] joint hidden state
+  void* A = nullptr;       // [cap_seq L, H] modulated block input
+  void* Y = nullptr;       // [cap_seq L, 4H+F]: q | k | v | attn out | mlp hidden
+  void* vt = nullptr;      // bf16 [cap_seq, heads, 128, round_up(L, 64)]
+  float* modq = nullptr;   // f32 [cap_seq, n_mod]: gathered modulation vectors of one step
   void* yf = nullptr;      // [N, H] final-layer input
   float* vel = nullptr;    // f32 [nb, N, C]
-  float* x_last = nullptr; // f32 [N, C]: UniPC's corrected sample of the previous step
-  float* mh[3] = {nullptr, nullptr, nullptr};  // f32 [N, C]: UniPC data predictions (rotating)
-  void* txt = nullptr;     // [nb, Nt, H]
   void* ctxkv = nullptr;   // [Nt, 2H] cross-attention k | v
   void* vt2 = nullptr;     // bf16 [heads, 128, round_up(Nt, 64)]
   float* ones = nullptr;   // f32 [H] (ungated residual)
   double* partials = nullptr;
   int max_partials = 0;
-  double* sums_host = nullptr;  // pinned, mapped [4]
+  double* sums_host = nullptr;  // pinned, mapped [lanes, 4]
   double* sums_dev = nullptr;
+  int cap_sums = 0;
   hipEvent_t ev_sums = nullptr;
 
-  // per-sample buffers, grown on demand (sized by T)
-  int cap_T = 0;
-  float* mod = nullptr;    // f32 [nb, T, n_mod]
-  float* modx = nullptr;   // f32 [nb, n_cross, T, 6H]
+  // per-call tables, grown on demand (sized by T and the modulation slots:
+  // one per branch of each sample with pooled text, else one)
+  int cap_T = 0, cap_slots = 0;
+  float* mod = nullptr;    // f32 [slots, T, n_mod]
+  float* modx = nullptr;   // f32 [slots, n_cross, T, 6H]
   void* temb = nullptr;    // [T, time_dim]
   void* th = nullptr;      // [T, H]
   float* tv = nullptr;     // f32 [T, H]
@@ -240,31 +253,34 @@ dit_status typed(dit_cache* c, Fn fn) {
 }
 
 dit_status ln_mod(dit_cache* c, const void* x, int64_t ldx, void* out, int64_t ldo, int rows, int split,
-                  const float* sh0, const float* sc0, const float* sh1, const float* sc1, int cls) {
+                  const float* sh0, const float* sc0, const float* sh1, const float* sc1, int cls,
+                  int seg0 = 0x7fffffff, int seg1 = 0x7fffffff, int64_t mstride = 0) {
   Scope s(c, cls, 2.0 * rows * c->H * c->esz);
   return typed(c, [&](auto* tp) {
     using T = std::remove_pointer_t<decltype(tp)>;
     return dit::launch_ln_mod<T>((const T*)x, ldx, (T*)out, ldo, rows, c->H, split, sh0, sc0, sh1, sc1,
-                                 c->stream);
+                                 c->stream, seg0, seg1, mstride);
   });
 }
 
-// attention over joint rows: q,k,v inside Y (or separate), output into o
+// attention over joint rows: q,k,v inside Y (or separate), output into o;
+// nseq stacked sequences in one launch (bf16; see launch_flash_attn_bf16)
 dit_status attention(dit_cache* c, const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v,
                      int64_t ldv, void* o, int64_t ldo, int Lq, int Lk, void* vt_ws, int split = 0x7fffffff,
-                     int64_t gap = 0) {
+                     int64_t gap = 0, int nseq = 1, int64_t zs = 0, int64_t gz = 0) {
   const int heads = c->cfg.heads, hd = c->cfg.head_dim;
-  const double flops = 4.0 * Lq * (double)Lk * heads * hd;
+  const double flops = 4.0 * Lq * (double)Lk * heads * hd * nseq;
   if (c->bf16) {
     {
-      Scope s(c, DIT_K_FULL_OTHER, 2.0 * Lk * heads * hd * 2);
-      HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt_ws, Lk, heads, c->stream, split, gap));
+      Scope s(c, DIT_K_FULL_OTHER, 2.0 * Lk * heads * hd * 2 * nseq);
+      HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt_ws, Lk, heads, c->stream, split, gap, nseq, zs, gz));
     }
     Scope s(c, DIT_K_ATTN, flops);
     // q and k leave the projection through a unit-gain RMS norm: bounded logits
     HIPCK(dit::launch_flash_attn_bf16(q, ldq, k, ldk, vt_ws, (int)rup(Lk, 64), o, ldo, Lq, Lk, heads,
-                                      true, c->stream, split, gap));
+                                      true, c->stream, split, gap, nseq, zs, gz));
   } else {
+    if (nseq != 1) return fail(c, DIT_EINVAL, "f32 attention runs one sequence per launch");
     Scope s(c, DIT_K_ATTN, flops);
     HIPCK(dit::launch_attn_f32((const float*)q, ldq, (const float*)k, ldk, (const float*)v, ldv,
                                (float*)o, ldo, Lq, Lk, heads, hd, c->stream));
@@ -356,23 +372,74 @@ dit_status dalloc(dit_cache* c, P** p, size_t bytes) {
   return DIT_OK;
 }
 
+void free_lane(Lane& l) {
+  void* ps[] = {l.h, l.mbuf[0], l.mbuf[1], l.mbuf[2], l.r, l.txt, l.x_last, l.mh[0], l.mh[1], l.mh[2]};
+  for (void* p : ps)
+    if (p) hipFree(p);
+  l = Lane{};
+}
+
+dit_status alloc_lane(dit_cache* c, Lane& l) {
+  const size_t e = c->esz;
+  const size_t NH = (size_t)c->N * c->H, NC = (size_t)c->N * c->C;
+  TRY(dalloc(c, &l.h, NH * e));
+  for (auto& m : l.mbuf) TRY(dalloc(c, &m, NH * e));
+  TRY(dalloc(c, &l.r, c->nb * NH * e));
+  TRY(dalloc(c, &l.txt, (size_t)c->nb * c->Nt * c->H * e));
+  TRY(dalloc(c, &l.x_last, NC * 4));
+  for (auto& m : l.mh) TRY(dalloc(c, &m, NC * 4));
+  return DIT_OK;
+}
+
+// Block-stack workspace for Q sequences (stacked: Q L rows; else one).
+dit_status ensure_seq(dit_cache* c, int Q) {
+  if (!c->stacked) Q = 1;
+  if (Q <= c->cap_seq) return DIT_OK;
+  for (void* p : {c->X, c->A, c->Y, c->vt, (void*)c->modq})
+    if (p) hipFree(p);
+  c->X = c->A = c->Y = c->vt = nullptr;
+  c->modq = nullptr;
+  c->cap_seq = 0;
+  const size_t e = c->esz, LB = (size_t)c->L * Q;
+  TRY(dalloc(c, &c->X, LB * c->H * e));
+  TRY(dalloc(c, &c->A, LB * c->H * e));
+  TRY(dalloc(c, &c->Y, LB * c->ldY * e));
+  if (c->bf16) TRY(dalloc(c, &c->vt, (size_t)Q * c->cfg.heads * 128 * rup(c->L, 64) * 2));
+  if (c->stacked && c->cfg.pooled_text) TRY(dalloc(c, &c->modq, (size_t)Q * c->n_mod * 4));
+  c->cap_seq = Q;
+  return DIT_OK;
+}
+
+// S sample lanes, the pinned indicator sums of each and the stack workspace
+// for all their sequences.
+dit_status ensure_lanes(dit_cache* c, int S) {
+  while ((int)c->lanes.size() < S) {
+    c->lanes.emplace_back();
+    dit_status st = alloc_lane(c, c->lanes.back());
+    if (st != DIT_OK) {
+      free_lane(c->lanes.back());
+      c->lanes.pop_back();
+      return st;
+    }
+  }
+  if (S > c->cap_sums) {
+    if (c->sums_host) hipHostFree(c->sums_host);
+    c->sums_host = c->sums_dev = nullptr;
+    c->cap_sums = 0;
+    if (hipHostMalloc((void**)&c->sums_host, (size_t)S * 4 * sizeof(double), hipHostMallocMapped) != hipSuccess)
+      return fail(c, DIT_ENOMEM, "pinned host allocation failed");
+    HIPCK(hipHostGetDevicePointer((void**)&c->sums_dev, c->sums_host, 0));
+    c->cap_sums = S;
+  }
+  return ensure_seq(c, S * c->nb);
+}
+
 dit_status alloc_workspace(dit_cache* c) {
   const size_t e = c->esz;
-  const int H = c->H, N = c->N, L = c->L, Nt = c->Nt;
+  const int H = c->H, N = c->N, Nt = c->Nt;
   TRY(dalloc(c, &c->xs, (size_t)N * c->C * e));
-  TRY(dalloc(c, &c->h, (size_t)N * H * e));
-  for (auto& m : c->mbuf) TRY(dalloc(c, &m, (size_t)N * H * e));
-  TRY(dalloc(c, &c->r, (size_t)c->nb * N * H * e));
-  const size_t LB = (size_t)L * (c->pair_batched ? c->nb : 1);  // block-stack rows
-  TRY(dalloc(c, &c->X, LB * H * e));
-  TRY(dalloc(c, &c->A, LB * H * e));
-  TRY(dalloc(c, &c->Y, LB * c->ldY * e));
-  if (c->bf16) TRY(dalloc(c, &c->vt, (size_t)c->cfg.heads * 128 * rup(L, 64) * 2));
   TRY(dalloc(c, &c->yf, (size_t)N * H * e));
   TRY(dalloc(c, &c->vel, (size_t)c->nb * N * c->C * 4));
-  TRY(dalloc(c, &c->x_last, (size_t)N * c->C * 4));
-  for (auto& m : c->mh) TRY(dalloc(c, &m, (size_t)N * c->C * 4));
-  TRY(dalloc(c, &c->txt, (size_t)c->nb * Nt * H * e));
   if (c->cfg.n_cross) {
     TRY(dalloc(c, &c->ctxkv, (size_t)Nt * 2 * H * e));
     if (c->bf16) TRY(dalloc(c, &c->vt2, (size_t)c->cfg.heads * 128 * rup(Nt, 64) * 2));
@@ -384,29 +451,31 @@ dit_status alloc_workspace(dit_cache* c) {
   }
   c->max_partials = std::max(dit::indicator_partials(N), dit::reuse_indicator_partials(N));
   TRY(dalloc(c, &c->partials, (size_t)c->max_partials * 4 * sizeof(double)));
-  HIPCK(hipHostMalloc((void**)&c->sums_host, 4 * sizeof(double), hipHostMallocMapped));
-  HIPCK(hipHostGetDevicePointer((void**)&c->sums_dev, c->sums_host, 0));
   HIPCK(hipEventCreateWithFlags(&c->ev_sums, hipEventDisableTiming));
-  return DIT_OK;
+  return ensure_lanes(c, 1);
 }
 
-void free_per_sample(dit_cache* c) {
+void free_per_call(dit_cache* c) {
   void* ps[] = {c->mod, c->modx, c->temb, c->th, c->tv, c->pooled, c->ph, c->pv, c->svec, c->sig_dev};
   for (void* p : ps)
     if (p) hipFree(p);
   c->mod = c->modx = c->tv = c->pv = nullptr;
   c->temb = c->th = c->pooled = c->ph = c->svec = nullptr;
   c->sig_dev = nullptr;
-  c->cap_T = 0;
+  c->cap_T = c->cap_slots = 0;
 }
 
-dit_status ensure_T(dit_cache* c, int T) {
-  if (T <= c->cap_T) return DIT_OK;
-  free_per_sample(c);
+int mod_slots(const dit_cache* c, int S) { return c->cfg.pooled_text ? S * c->nb : 1; }
+
+dit_status ensure_T(dit_cache* c, int T, int S) {
+  const int slots = mod_slots(c, S);
+  if (T <= c->cap_T && slots <= c->cap_slots) return DIT_OK;
+  T = std::max(T, c->cap_T);
+  free_per_call(c);
   const size_t e = c->esz;
   const int H = c->H;
-  TRY(dalloc(c, &c->mod, (size_t)c->nb * T * c->n_mod * 4));
-  if (c->cfg.n_cross) TRY(dalloc(c, &c->modx, (size_t)c->nb * c->cfg.n_cross * T * 6 * H * 4));
+  TRY(dalloc(c, &c->mod, (size_t)slots * T * c->n_mod * 4));
+  if (c->cfg.n_cross) TRY(dalloc(c, &c->modx, (size_t)slots * c->cfg.n_cross * T * 6 * H * 4));
   TRY(dalloc(c, &c->temb, (size_t)T * c->cfg.time_dim * e));
   TRY(dalloc(c, &c->th, (size_t)T * H * e));
   TRY(dalloc(c, &c->tv, (size_t)T * H * 4));
@@ -416,6 +485,7 @@ dit_status ensure_T(dit_cache* c, int T) {
   TRY(dalloc(c, &c->svec, (size_t)T * H * e));
   TRY(dalloc(c, &c->sig_dev, (size_t)(T + 1) * sizeof(double)));
   c->cap_T = T;
+  c->cap_slots = slots;
   return DIT_OK;
 }
 
@@ -528,26 +598,29 @@ double gate_logit(const GateMLP& g, const double* f) {
 }
 
 // ---------------------------------------------------------------- steps
-struct StepCtx {
-  int t, T;
-  const float* modp[2];   // this step's modulation vector per branch
-  const float* modxp[2];  // video blocks: base of [n_cross][T][6H] per branch
+// One sequence through the block stack: one branch of one sample.
+struct Seq {
+  const void* txt;    // [Nt, H] projected text tokens
+  const void* h;      // [N, H] image-token input
+  void* r;            // [N, H] refreshed residual (out)
+  const float* mod;   // this step's modulation vector [n_mod]
+  const float* modx;  // video blocks: base of [n_cross][T][6H]
 };
 
-dit_status full_stack(dit_cache* c, int b, const StepCtx& s) {
-  const int H = c->H, F = c->F, N = c->N, Nt = c->Nt, L = c->L, ldY = c->ldY;
-  const float* md = s.modp[b];
-  const void* txtb = sp(c, c->txt, (size_t)b * Nt * H);
+// One sequence at a time (f32 storage, video blocks).
+dit_status full_stack(dit_cache* c, const Seq& q, int t, int T) {
+  const int H = c->H, N = c->N, Nt = c->Nt, L = c->L, ldY = c->ldY;
+  const float* md = q.mod;
   char* Xi = sp(c, c->X, (size_t)Nt * H);  // image rows of the joint state
   char* Ai = sp(c, c->A, (size_t)Nt * H);
   char* Yi = sp(c, c->Y, (size_t)Nt * ldY);
   const int cls = DIT_K_GEMM;
 
   if (c->cfg.n_cross) {
-    HIPCK(hipMemcpyAsync(c->X, c->h, (size_t)N * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
+    HIPCK(hipMemcpyAsync(c->X, q.h, (size_t)N * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
     for (int i = 0; i < c->cfg.n_cross; ++i) {
       const CrossW& w = c->M.crs[i];
-      const float* e = s.modxp[b] + ((size_t)i * s.T + s.t) * 6 * H;
+      const float* e = q.modx + ((size_t)i * T + t) * 6 * H;
       TRY(ln_mod(c, c->X, H, c->A, H, N, N, e, e + H, e, e + H, DIT_K_FULL_OTHER));
       GemmArgs g = lin_args(c, c->A, H, w.qkv, c->Y, ldY, N);
       g.rms_cols = 2 * H;
@@ -561,7 +634,7 @@ dit_status full_stack(dit_cache* c, int b, const StepCtx& s) {
       TRY(ln_mod(c, c->X, H, c->A, H, N, N, nullptr, nullptr, nullptr, nullptr, DIT_K_FULL_OTHER));
       GemmArgs gq = lin_args(c, c->A, H, w.xq, c->Y, ldY, N);
       gq.rms_cols = H;
-      GemmArgs gkv = lin_args(c, txtb, H, w.xkv, c->ctxkv, 2 * H, Nt);
+      GemmArgs gkv = lin_args(c, q.txt, H, w.xkv, c->ctxkv, 2 * H, Nt);
       gkv.rms_cols = H;
       TRY(gemm(c, &gq, 1, cls));
       TRY(gemm(c, &gkv, 1, cls));
@@ -581,17 +654,16 @@ dit_status full_stack(dit_cache* c, int b, const StepCtx& s) {
     {
       Scope sc(c, DIT_K_FULL_OTHER, 3.0 * N * H * c->esz);
       TRY(typed(c, [&](auto* tp) {
-        using T = std::remove_pointer_t<decltype(tp)>;
-        return dit::launch_add<T>((const T*)c->X, (const T*)c->h, (T*)sp(c, c->r, (size_t)b * N * H),
-                                  (int64_t)N * H, -1.f, c->stream);
+        using T_ = std::remove_pointer_t<decltype(tp)>;
+        return dit::launch_add<T_>((const T_*)c->X, (const T_*)q.h, (T_*)q.r, (int64_t)N * H, -1.f, c->stream);
       }));
     }
     return DIT_OK;
   }
 
   // MMDiT: X = [txt; img]
-  HIPCK(hipMemcpyAsync(c->X, txtb, (size_t)Nt * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
-  HIPCK(hipMemcpyAsync(Xi, c->h, (size_t)N * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
+  HIPCK(hipMemcpyAsync(c->X, q.txt, (size_t)Nt * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
+  HIPCK(hipMemcpyAsync(Xi, q.h, (size_t)N * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
   for (int i = 0; i < c->cfg.n_double; ++i) {
     const DoubleW& w = c->M.dbl[i];
     const float* mi = md + (size_t)12 * H * i;  // image stream chunk
@@ -639,87 +711,141 @@ dit_status full_stack(dit_cache* c, int b, const StepCtx& s) {
   {
     Scope sc(c, DIT_K_FULL_OTHER, 3.0 * N * H * c->esz);
     TRY(typed(c, [&](auto* tp) {
-      using T = std::remove_pointer_t<decltype(tp)>;
-      return dit::launch_add<T>((const T*)Xi, (const T*)c->h, (T*)sp(c, c->r, (size_t)b * N * H),
-                                (int64_t)N * H, -1.f, c->stream);
+      using T_ = std::remove_pointer_t<decltype(tp)>;
+      return dit::launch_add<T_>((const T_*)Xi, (const T_*)q.h, (T_*)q.r, (int64_t)N * H, -1.f, c->stream);
     }));
   }
-  (void)F;
   return DIT_OK;
 }
 
-// Both branches of a guidance pair through the MMDiT stack at once (bf16, one
-// modulation table for both).  Rows are stream-major, [txt_0; txt_1; img_0;
-// img_1], so each linear layer is one launch over both branches' rows of a
-// stream (twice the rows per weight read); attention runs per branch on its
-// two row pieces (text rows, then image rows nb Nt + b N rows down).
-dit_status full_stack_pair(dit_cache* c, const StepCtx& s) {
-  const int H = c->H, N = c->N, Nt = c->Nt, L = c->L, ldY = c->ldY, nb = c->nb;
-  const int Lt = nb * Nt, Li = nb * N, LL = nb * L;
-  const float* md = s.modp[0];
+// Modulation vectors of the Q stacked sequences: sequence q's at base + q d
+// (d = 0: one vector shared by all).
+struct ModRef {
+  const float* base;
+  int64_t d;
+};
+
+// Q sequences through the MMDiT stack at once (bf16).  Rows are
+// stream-major, [txt_0; ...; txt_{Q-1}; img_0; ...; img_{Q-1}], so each
+// linear layer is one launch over every sequence's rows of a stream (Q
+// times the rows per weight read); attention is one launch over the Q
+// sequences, each read as its two row pieces.  Modulation vectors are per
+// sequence (pooled text) or shared.
+dit_status full_stack_multi(dit_cache* c, const Seq* seqs, int Q) {
+  const int H = c->H, N = c->N, Nt = c->Nt, L = c->L, ldY = c->ldY;
+  const int Lt = Q * Nt, Li = Q * N, LL = Q * L;
+  const size_t es = c->esz;
   char* Xi = sp(c, c->X, (size_t)Lt * H);
   char* Ai = sp(c, c->A, (size_t)Lt * H);
   char* Yi = sp(c, c->Y, (size_t)Lt * ldY);
   const int cls = DIT_K_GEMM;
-  for (int b = 0; b < nb; ++b) {
-    HIPCK(hipMemcpyAsync(sp(c, c->X, (size_t)b * Nt * H), sp(c, c->txt, (size_t)b * Nt * H),
-                         (size_t)Nt * H * c->esz, hipMemcpyDeviceToDevice, c->stream));
-    HIPCK(hipMemcpyAsync(sp(c, Xi, (size_t)b * N * H), c->h, (size_t)N * H * c->esz, hipMemcpyDeviceToDevice,
+  for (int q = 0; q < Q; ++q) {
+    HIPCK(hipMemcpyAsync(sp(c, c->X, (size_t)q * Nt * H), seqs[q].txt, (size_t)Nt * H * es,
+                         hipMemcpyDeviceToDevice, c->stream));
+    HIPCK(hipMemcpyAsync(sp(c, Xi, (size_t)q * N * H), seqs[q].h, (size_t)N * H * es, hipMemcpyDeviceToDevice,
                          c->stream));
   }
-  // branch b's joint sequence: text rows from row b Nt, image rows from row Lt + b N
-  auto attn_b = [&](int b) {
-    const char* y0 = sp(c, c->Y, (size_t)b * Nt * ldY);
-    const int64_t gap = (int64_t)(nb - 1 - b) * Nt + (int64_t)b * N;
-    return attention(c, y0, ldY, y0 + (size_t)H * c->esz, ldY, y0 + (size_t)2 * H * c->esz, ldY,
-                     (void*)(y0 + (size_t)3 * H * c->esz), ldY, L, L, c->vt, Nt, gap);
+  // the sequences' modulation vectors as base + q d: shared, evenly spaced,
+  // or gathered into modq
+  ModRef mr{seqs[0].mod, 0};
+  if (Q > 1) {
+    mr.d = seqs[1].mod - seqs[0].mod;
+    bool even = true;
+    for (int q = 2; q < Q; ++q) even &= seqs[q].mod - seqs[0].mod == q * mr.d;
+    if (!even) {
+      for (int q = 0; q < Q; ++q)
+        HIPCK(hipMemcpyAsync(c->modq + (size_t)q * c->n_mod, seqs[q].mod, (size_t)c->n_mod * 4,
+                             hipMemcpyDeviceToDevice, c->stream));
+      mr = ModRef{c->modq, c->n_mod};
+    }
+  }
+  // per-segment gate vectors in the GEMM need 32 | segment rows; otherwise
+  // the gated layers run per sequence
+  const bool seg_gemm = mr.d == 0 || (N % 32 == 0 && Nt % 32 == 0);
+  // gated residual over the image rows (gi, column offset oi of the
+  // modulation vector) and the text rows (gt, offset ot) of every sequence
+  auto gated = [&](GemmArgs gi, GemmArgs gt, size_t oi, size_t ot) -> dit_status {
+    gi.gate = mr.base + oi;
+    gt.gate = mr.base + ot;
+    if (mr.d == 0 || seg_gemm) {
+      if (mr.d) {
+        gi.gseg = N; gt.gseg = Nt;
+        gi.gstride = gt.gstride = mr.d;
+      }
+      GemmArgs g[2] = {gi, gt};
+      return gemm(c, g, 2, cls);
+    }
+    for (int q = 0; q < Q; ++q) {
+      GemmArgs g[2] = {gi, gt};
+      g[0].A = sp(c, gi.A, (size_t)q * N * gi.lda);
+      g[0].C = sp(c, gi.C, (size_t)q * N * gi.ldc);
+      g[0].M = N;
+      g[0].gate = mr.base + q * mr.d + oi;
+      g[1].A = sp(c, gt.A, (size_t)q * Nt * gt.lda);
+      g[1].C = sp(c, gt.C, (size_t)q * Nt * gt.ldc);
+      g[1].M = Nt;
+      g[1].gate = mr.base + q * mr.d + ot;
+      TRY(gemm(c, g, 2, cls));
+    }
+    return DIT_OK;
+  };
+  // adaLN over all rows: text rows take offset ot, image rows oi
+  auto lnm = [&](size_t ot, size_t oi) {
+    const float* b = mr.base;
+    return ln_mod(c, c->X, H, c->A, H, LL, Lt, b + ot, b + ot + H, b + oi, b + oi + H, DIT_K_FULL_OTHER, Nt, N,
+                  mr.d);
+  };
+  auto attn = [&]() {
+    return attention(c, c->Y, ldY, sp(c, c->Y, H), ldY, sp(c, c->Y, 2 * H), ldY, sp(c, c->Y, 3 * H), ldY, L, L,
+                     c->vt, Nt, (int64_t)(Q - 1) * Nt, Q, Nt, (int64_t)N - Nt);
   };
   for (int i = 0; i < c->cfg.n_double; ++i) {
     const DoubleW& w = c->M.dbl[i];
-    const float* mi = md + (size_t)12 * H * i;
-    const float* mt = mi + 6 * H;
-    TRY(ln_mod(c, c->X, H, c->A, H, LL, Lt, mt, mt + H, mi, mi + H, DIT_K_FULL_OTHER));
+    const size_t mi = (size_t)12 * H * i, mt = mi + 6 * H;  // image / text stream chunks
+    TRY(lnm(mt, mi));
     GemmArgs g[2];
     g[0] = lin_args(c, Ai, H, w.qkv[0], Yi, ldY, Li);
     g[1] = lin_args(c, c->A, H, w.qkv[1], c->Y, ldY, Lt);
     g[0].rms_cols = g[1].rms_cols = 2 * H;
     TRY(gemm(c, g, 2, cls));
-    for (int b = 0; b < nb; ++b) TRY(attn_b(b));
-    g[0] = lin_args(c, Yi + 3 * H * c->esz, ldY, w.o[0], Xi, H, Li, DIT_EPI_GATED_RES);
-    g[1] = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.o[1], c->X, H, Lt, DIT_EPI_GATED_RES);
-    g[0].gate = mi + 2 * H;
-    g[1].gate = mt + 2 * H;
-    TRY(gemm(c, g, 2, cls));
-    TRY(ln_mod(c, c->X, H, c->A, H, LL, Lt, mt + 3 * H, mt + 4 * H, mi + 3 * H, mi + 4 * H, DIT_K_FULL_OTHER));
-    g[0] = lin_args(c, Ai, H, w.mlp0[0], Yi + 4 * H * c->esz, ldY, Li);
+    TRY(attn());
+    TRY(gated(lin_args(c, Yi + 3 * H * es, ldY, w.o[0], Xi, H, Li, DIT_EPI_GATED_RES),
+              lin_args(c, sp(c, c->Y, 3 * H), ldY, w.o[1], c->X, H, Lt, DIT_EPI_GATED_RES), mi + 2 * H,
+              mt + 2 * H));
+    TRY(lnm(mt + 3 * H, mi + 3 * H));
+    g[0] = lin_args(c, Ai, H, w.mlp0[0], Yi + 4 * H * es, ldY, Li);
     g[1] = lin_args(c, c->A, H, w.mlp0[1], sp(c, c->Y, 4 * H), ldY, Lt);
     g[0].gelu_from = g[1].gelu_from = 0;
     TRY(gemm(c, g, 2, cls));
-    g[0] = lin_args(c, Yi + 4 * H * c->esz, ldY, w.mlp1[0], Xi, H, Li, DIT_EPI_GATED_RES);
-    g[1] = lin_args(c, sp(c, c->Y, 4 * H), ldY, w.mlp1[1], c->X, H, Lt, DIT_EPI_GATED_RES);
-    g[0].gate = mi + 5 * H;
-    g[1].gate = mt + 5 * H;
-    TRY(gemm(c, g, 2, cls));
+    TRY(gated(lin_args(c, Yi + 4 * H * es, ldY, w.mlp1[0], Xi, H, Li, DIT_EPI_GATED_RES),
+              lin_args(c, sp(c, c->Y, 4 * H), ldY, w.mlp1[1], c->X, H, Lt, DIT_EPI_GATED_RES), mi + 5 * H,
+              mt + 5 * H));
   }
   for (int i = 0; i < c->cfg.n_single; ++i) {
     const SingleW& w = c->M.sgl[i];
-    const float* ms = md + (size_t)12 * H * c->cfg.n_double + (size_t)3 * H * i;
-    TRY(ln_mod(c, c->X, H, c->A, H, LL, LL, ms, ms + H, ms, ms + H, DIT_K_FULL_OTHER));
+    const size_t ms = (size_t)12 * H * c->cfg.n_double + (size_t)3 * H * i;
+    TRY(lnm(ms, ms));
     GemmArgs g = lin_args(c, c->A, H, w.l1, c->Y, ldY, LL);
     g.rms_cols = 2 * H;
     g.gelu_from = 3 * H;
     g.gap_at = 3 * H;
     g.gap = H;
     TRY(gemm(c, &g, 1, cls));
-    for (int b = 0; b < nb; ++b) TRY(attn_b(b));
-    g = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.l2, c->X, H, LL, DIT_EPI_GATED_RES);
-    g.gate = ms + 2 * H;
-    TRY(gemm(c, &g, 1, cls));
+    TRY(attn());
+    if (mr.d == 0) {
+      g = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.l2, c->X, H, LL, DIT_EPI_GATED_RES);
+      g.gate = mr.base + ms + 2 * H;
+      TRY(gemm(c, &g, 1, cls));
+    } else {
+      TRY(gated(lin_args(c, Yi + 3 * H * es, ldY, w.l2, Xi, H, Li, DIT_EPI_GATED_RES),
+                lin_args(c, sp(c, c->Y, 3 * H), ldY, w.l2, c->X, H, Lt, DIT_EPI_GATED_RES), ms + 2 * H,
+                ms + 2 * H));
+    }
   }
-  for (int b = 0; b < nb; ++b) {
-    Scope sc(c, DIT_K_FULL_OTHER, 3.0 * N * H * c->esz);
-    HIPCK(dit::launch_add<bf16_t>((const bf16_t*)sp(c, Xi, (size_t)b * N * H), (const bf16_t*)c->h,
-                                  (bf16_t*)sp(c, c->r, (size_t)b * N * H), (int64_t)N * H, -1.f, c->stream));
+  for (int q = 0; q < Q; ++q) {
+    Scope sc(c, DIT_K_FULL_OTHER, 3.0 * N * H * es);
+    HIPCK(dit::launch_add<bf16_t>((const bf16_t*)sp(c, Xi, (size_t)q * N * H), (const bf16_t*)seqs[q].h,
+                                  (bf16_t*)seqs[q].r, (int64_t)N * H, -1.f, c->stream));
   }
   return DIT_OK;
 }
@@ -749,16 +875,20 @@ dit_status final_project(dit_cache* c, int b, int cls, float* latent = nullptr, 
 }
 
 // full step: y = S(LN(h_out)(1+scale_f)+shift_f), then the projection
-dit_status final_layer(dit_cache* c, int b, const void* hout, const StepCtx& s, int cls, float* latent = nullptr,
+dit_status final_layer(dit_cache* c, int b, const void* hout, const float* mod, int cls, float* latent = nullptr,
                        float dsig = 0.f) {
   const int H = c->H, N = c->N;
-  const float* mf = s.modp[b] + (c->n_mod - 2 * H);
+  const float* mf = mod + (c->n_mod - 2 * H);
   TRY(ln_mod(c, hout, H, c->yf, H, N, N, mf, mf + H, mf, mf + H, cls));
   return final_project(c, b, cls, latent, dsig);
 }
 
-// once per sample: text tokens, vec and the modulation table of every step
-dit_status prepare(dit_cache* c, const void* text_emb, const std::vector<double>& sig, int T) {
+// Modulation table slot of branch b of sample j.
+int mod_slot(const dit_cache* c, int j, int b) { return c->cfg.pooled_text ? j * c->nb + b : 0; }
+
+// once per call: text tokens of every sample, vec and the modulation table
+// of every step (one per branch and sample with pooled text, else one)
+dit_status prepare(dit_cache* c, int S, const void* text_emb, const std::vector<double>& sig, int T) {
   const int H = c->H, Nt = c->Nt, X = c->cfg.ctx_dim;
   const int cls = DIT_K_ONCE;
   HIPCK(hipMemcpyAsync(c->sig_dev, sig.data(), (T + 1) * sizeof(double), hipMemcpyHostToDevice, c->stream));
@@ -773,48 +903,51 @@ dit_status prepare(dit_cache* c, const void* text_emb, const std::vector<double>
   TRY(gemm(c, &g, 1, cls));
   g = lin_args(c, c->th, H, c->M.time2, c->tv, H, T, DIT_EPI_F32);
   TRY(gemm(c, &g, 1, cls));
-  for (int b = 0; b < c->nb; ++b) {
-    const void* te = (const char*)text_emb + (size_t)b * Nt * X * c->esz;
-    g = lin_args(c, te, X, c->M.txt_in, sp(c, c->txt, (size_t)b * Nt * H), H, Nt);
-    TRY(gemm(c, &g, 1, cls));
-    if (b > 0 && !c->cfg.pooled_text) continue;  // identical vec and mod table
-    const float* pvp = nullptr;
-    if (c->cfg.pooled_text) {
+  for (int j = 0; j < S; ++j)
+    for (int b = 0; b < c->nb; ++b) {
+      const void* te = (const char*)text_emb + ((size_t)j * c->nb + b) * Nt * X * c->esz;
+      g = lin_args(c, te, X, c->M.txt_in, sp(c, c->lanes[j].txt, (size_t)b * Nt * H), H, Nt);
+      TRY(gemm(c, &g, 1, cls));
+      if ((j > 0 || b > 0) && !c->cfg.pooled_text) continue;  // identical vec and mod table
+      const int slot = mod_slot(c, j, b);
+      const float* pvp = nullptr;
+      if (c->cfg.pooled_text) {
+        {
+          Scope s(c, cls, 0);
+          TRY(typed(c, [&](auto* tp) {
+            using Ty = std::remove_pointer_t<decltype(tp)>;
+            return dit::launch_mean_rows<Ty>((const Ty*)te, Nt, X, (Ty*)c->pooled, c->stream);
+          }));
+        }
+        g = lin_args(c, c->pooled, X, c->M.pool0, c->ph, H, 1, DIT_EPI_SILU);
+        TRY(gemm(c, &g, 1, cls));
+        g = lin_args(c, c->ph, H, c->M.pool2, c->pv, H, 1, DIT_EPI_F32);
+        TRY(gemm(c, &g, 1, cls));
+        pvp = c->pv;
+      }
       {
         Scope s(c, cls, 0);
         TRY(typed(c, [&](auto* tp) {
           using Ty = std::remove_pointer_t<decltype(tp)>;
-          return dit::launch_mean_rows<Ty>((const Ty*)te, Nt, X, (Ty*)c->pooled, c->stream);
+          return dit::launch_vec_silu<Ty>(c->tv, pvp, (Ty*)c->svec, T, H, c->stream);
         }));
       }
-      g = lin_args(c, c->pooled, X, c->M.pool0, c->ph, H, 1, DIT_EPI_SILU);
+      float* mod = c->mod + (size_t)slot * T * c->n_mod;
+      g = lin_args(c, c->svec, H, c->M.mod, mod, c->n_mod, T, DIT_EPI_F32);
       TRY(gemm(c, &g, 1, cls));
-      g = lin_args(c, c->ph, H, c->M.pool2, c->pv, H, 1, DIT_EPI_F32);
-      TRY(gemm(c, &g, 1, cls));
-      pvp = c->pv;
-    }
-    {
-      Scope s(c, cls, 0);
-      TRY(typed(c, [&](auto* tp) {
-        using Ty = std::remove_pointer_t<decltype(tp)>;
-        return dit::launch_vec_silu<Ty>(c->tv, pvp, (Ty*)c->svec, T, H, c->stream);
-      }));
-    }
-    g = lin_args(c, c->svec, H, c->M.mod, c->mod + (size_t)b * T * c->n_mod, c->n_mod, T, DIT_EPI_F32);
-    TRY(gemm(c, &g, 1, cls));
-    if (c->cfg.n_cross) {
-      const int base = 12 * H * c->cfg.n_double + 3 * H * c->cfg.n_single;
-      for (int i = 0; i < c->cfg.n_cross; ++i) {
-        Scope s(c, cls, 0);
-        float* dst = c->modx + ((size_t)b * c->cfg.n_cross + i) * T * 6 * H;
-        TRY(typed(c, [&](auto* tp) {
-          using Ty = std::remove_pointer_t<decltype(tp)>;
-          return dit::launch_add_offset<Ty>(c->mod + (size_t)b * T * c->n_mod, c->n_mod, base,
-                                            (const Ty*)c->M.crs[i].mod_off, dst, T, 6 * H, c->stream);
-        }));
+      if (c->cfg.n_cross) {
+        const int base = 12 * H * c->cfg.n_double + 3 * H * c->cfg.n_single;
+        for (int i = 0; i < c->cfg.n_cross; ++i) {
+          Scope s(c, cls, 0);
+          float* dst = c->modx + ((size_t)slot * c->cfg.n_cross + i) * T * 6 * H;
+          TRY(typed(c, [&](auto* tp) {
+            using Ty = std::remove_pointer_t<decltype(tp)>;
+            return dit::launch_add_offset<Ty>(mod, c->n_mod, base, (const Ty*)c->M.crs[i].mod_off, dst, T, 6 * H,
+                                              c->stream);
+          }));
+        }
       }
     }
-  }
   return DIT_OK;
 }
 
@@ -887,10 +1020,14 @@ dit::UniCoef unipc_coef(const std::vector<double>& sig, int t, int T) {
   return k;
 }
 
-dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const GateMLP& gate,
-                      const dit_sample_params& p, dit_schedule* out) {
+// S samples in lockstep: each step runs (a1, a2) for every sample, one host
+// wait for all their sums, each sample's own decision (a3), then the reuse
+// samples (a4, a5) one by one and the computing ones' block stacks together.
+dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, const GateMLP& gate,
+                     const dit_sample_params& p, dit_schedule* out) {
   const int T = p.T, B = p.B;
-  const int H = c->H, N = c->N;
+  const int H = c->H, N = c->N, C = c->C, nb = c->nb;
+  const size_t NC = (size_t)N * C, NH = (size_t)N * H;
   std::vector<double> sig(T + 1);
   if (p.sigmas) {
     for (int i = 0; i <= T; ++i) sig[i] = p.sigmas[i];
@@ -900,197 +1037,242 @@ dit_status run_sample(dit_cache* c, float* latent, const void* text_emb, const G
       sig[i] = p.shift * u / (1.0 + (p.shift - 1.0) * u);
     }
   }
-  TRY(ensure_T(c, T));
-  TRY(prepare(c, text_emb, sig, T));
+  TRY(ensure_lanes(c, S));
+  TRY(ensure_T(c, T, S));
+  TRY(prepare(c, S, text_emb, sig, T));
 
-  StepCtx s{};
-  s.T = T;
-  const bool pair = c->nb == 2;
+  const bool pair = nb == 2;
+  const bool unipc = p.solver == DIT_SOLVER_UNIPC;
+  const bool fused = c->bf16 && dit::reuse_fused_fits(C, H);
+  const bool fused_euler = !pair && proj_fits(c) && !unipc;  // Euler folded into the projection
   const double thr = std::log(p.tau / (1.0 - p.tau));
   // mu(B, T) of the static policy: computed steps at floor(i T / B)
   std::vector<uint8_t> mu(T, 0);
   for (int i = 0; i < B; ++i) mu[(size_t)((int64_t)i * T / B)] = 1;
-  int cnt = 0, t_last = 0;
-  double acc = 0.0;
-  int i_prev = -1, i_last = -1;
-  out->nfe = 0;
-  out->steps_done = 0;
+  for (int j = 0; j < S; ++j) {
+    Lane& l = c->lanes[j];
+    l.cnt = 0; l.t_last = 0; l.acc = 0.0; l.i_prev = -1; l.i_last = -1; l.dec = true;
+    out[j].nfe = 0;
+    out[j].steps_done = 0;
+  }
+  auto modp = [&](int j, int b, int t) { return c->mod + ((size_t)mod_slot(c, j, b) * T + t) * c->n_mod; };
+  auto modxp = [&](int j, int b) {
+    return c->modx ? c->modx + (size_t)mod_slot(c, j, b) * c->cfg.n_cross * T * 6 * H : nullptr;
+  };
+  auto lat = [&](int j) { return latents + j * NC; };
+  auto fail_all = [&](int t, dit_status st, const std::string& m) {
+    for (int j = 0; j < S; ++j) out[j].steps_done = t;
+    return fail(c, st, m);
+  };
+  std::vector<Seq> seqs;
+  std::vector<int> comp;
 
   for (int t = 0; t < T; ++t) {
-    s.t = t;
-    for (int b = 0; b < c->nb; ++b) {
-      const int mb = (b > 0 && !c->cfg.pooled_text) ? 0 : b;
-      s.modp[b] = c->mod + ((size_t)mb * T + t) * c->n_mod;
-      s.modxp[b] = c->modx ? c->modx + (size_t)mb * c->cfg.n_cross * T * 6 * H : nullptr;
-    }
+    const float dsig = (float)(sig[t + 1] - sig[t]);
     // (a1) patch embed and modulated indicator tensor, (a2) its sums
-    int i_new = 0;
-    while (i_new == i_prev || i_new == i_last) ++i_new;
-    const float *sh0 = nullptr, *sc0 = nullptr;
-    if (p.indicator == DIT_INDICATOR_MODULATED) {
-      if (c->cfg.n_cross) {
-        sh0 = s.modxp[0] + (size_t)t * 6 * H;  // block 0
-        sc0 = sh0 + H;
-      } else {
-        sh0 = s.modp[0];  // first block's image-stream (or single) shift
+    for (int j = 0; j < S; ++j) {
+      Lane& l = c->lanes[j];
+      l.i_new = 0;
+      while (l.i_new == l.i_prev || l.i_new == l.i_last) ++l.i_new;
+      const float *sh0 = nullptr, *sc0 = nullptr;
+      if (p.indicator == DIT_INDICATOR_MODULATED) {
+        sh0 = c->cfg.n_cross ? modxp(j, 0) + (size_t)t * 6 * H  // block 0
+                             : modp(j, 0, t);                  // first block's image-stream (or single) shift
         sc0 = sh0 + H;
       }
-    }
-    const bool fused = c->bf16 && dit::reuse_fused_fits(c->C, H);
-    if (fused) {
-      // embedding recomputed in LDS: reads m_{t-1} and m_{t_last} (once if equal), writes m_t
-      Scope sc(c, DIT_K_INDICATOR, (double)N * H * c->esz * (t == 0 ? 1 : (i_prev == i_last ? 2 : 3)));
-      HIPCK(dit::launch_reuse_indicator(latent, c->C, c->M.img_in.w, c->M.img_in.b, c->mbuf[i_new],
-                                        t ? c->mbuf[i_prev] : nullptr, t ? c->mbuf[i_last] : nullptr, N, H,
-                                        sh0, sc0, t ? c->partials : nullptr, c->sums_dev, nullptr, c->stream));
-    } else {
-      Scope sc(c, DIT_K_INDICATOR, (double)N * H * c->esz * (t == 0 ? 2 : (i_prev == i_last ? 3 : 4)));
-      TRY(typed(c, [&](auto* tp) {
-        using Ty = std::remove_pointer_t<decltype(tp)>;
-        return dit::launch_cast_from_f32<Ty>(latent, (Ty*)c->xs, (int64_t)N * c->C, c->stream);
-      }));
-      GemmArgs g = lin_args(c, c->xs, c->C, c->M.img_in, c->h, H, N);
-      if (c->bf16) { HIPCK(dit::launch_gemm_bf16(&g, 1, c->stream, c->n_cu)); }
-      else { HIPCK(dit::launch_gemm_f32(&g, 1, c->stream)); }
-      TRY(typed(c, [&](auto* tp) {
-        using Ty = std::remove_pointer_t<decltype(tp)>;
-        return dit::launch_indicator<Ty>((const Ty*)c->h, (Ty*)c->mbuf[i_new],
-                                         t ? (const Ty*)c->mbuf[i_prev] : nullptr,
-                                         t ? (const Ty*)c->mbuf[i_last] : nullptr, N, H, sh0, sc0,
-                                         t ? c->partials : nullptr, c->sums_dev, c->stream);
-      }));
+      double* sums = c->sums_dev + 4 * j;
+      const void* mp = t ? l.mbuf[l.i_prev] : nullptr;
+      const void* ml = t ? l.mbuf[l.i_last] : nullptr;
+      if (fused) {
+        // embedding recomputed in LDS: reads m_{t-1} and m_{t_last} (once if equal), writes m_t
+        Scope sc(c, DIT_K_INDICATOR, (double)NH * c->esz * (t == 0 ? 1 : (l.i_prev == l.i_last ? 2 : 3)));
+        HIPCK(dit::launch_reuse_indicator(lat(j), C, c->M.img_in.w, c->M.img_in.b, l.mbuf[l.i_new], mp, ml, N, H,
+                                          sh0, sc0, t ? c->partials : nullptr, sums, nullptr, c->stream));
+      } else {
+        Scope sc(c, DIT_K_INDICATOR, (double)NH * c->esz * (t == 0 ? 2 : (l.i_prev == l.i_last ? 3 : 4)));
+        TRY(typed(c, [&](auto* tp) {
+          using Ty = std::remove_pointer_t<decltype(tp)>;
+          return dit::launch_cast_from_f32<Ty>(lat(j), (Ty*)c->xs, (int64_t)NC, c->stream);
+        }));
+        GemmArgs g = lin_args(c, c->xs, C, c->M.img_in, l.h, H, N);
+        if (c->bf16) { HIPCK(dit::launch_gemm_bf16(&g, 1, c->stream, c->n_cu)); }
+        else { HIPCK(dit::launch_gemm_f32(&g, 1, c->stream)); }
+        TRY(typed(c, [&](auto* tp) {
+          using Ty = std::remove_pointer_t<decltype(tp)>;
+          return dit::launch_indicator<Ty>((const Ty*)l.h, (Ty*)l.mbuf[l.i_new], (const Ty*)mp, (const Ty*)ml, N,
+                                           H, sh0, sc0, t ? c->partials : nullptr, sums, c->stream);
+        }));
+      }
     }
 
-    // (a3) gate + pacing on the host
-    int dec = 1, forced = 1;
-    double z = NAN;
-    double f[DIT_N_FEATURES];
-    for (double& v : f) v = NAN;
-    double sums[4] = {NAN, NAN, NAN, NAN};
+    // (a3) gate + pacing on the host, per sample, after one wait for all sums
     if (t > 0) {
       HIPCK(hipEventRecord(c->ev_sums, c->stream));
       HIPCK(hipEventSynchronize(c->ev_sums));
-      const auto h0 = std::chrono::steady_clock::now();
-      for (int k = 0; k < 4; ++k) sums[k] = ((volatile double*)c->sums_host)[k];
-      for (double v : sums)
-        if (!std::isfinite(v)) {
-          out->steps_done = t;
-          return fail(c, DIT_ENONFINITE, "indicator sum is not finite at step " + std::to_string(t));
+    }
+    const auto h0 = std::chrono::steady_clock::now();
+    comp.clear();
+    for (int j = 0; j < S; ++j) {
+      Lane& l = c->lanes[j];
+      int dec = 1, forced = 1;
+      double z = NAN;
+      double f[DIT_N_FEATURES];
+      for (double& v : f) v = NAN;
+      double sums[4] = {NAN, NAN, NAN, NAN};
+      if (t > 0) {
+        for (int k = 0; k < 4; ++k) sums[k] = ((volatile double*)c->sums_host)[4 * j + k];
+        for (double v : sums)
+          if (!std::isfinite(v))
+            return fail_all(t, DIT_ENONFINITE, "indicator sum is not finite at step " + std::to_string(t) +
+                                                   " of sample " + std::to_string(j));
+        const double d_prev = sums[0] / std::max(sums[1], 1e-30);
+        const double d_last = sums[2] / std::max(sums[3], 1e-30);
+        l.acc += d_prev;
+        f[0] = (double)B / T;
+        f[1] = (double)(B - l.cnt) / B;
+        f[2] = (double)(B - l.cnt) / (T - t);
+        f[3] = (double)(t - l.t_last);
+        f[4] = d_last;
+        f[5] = d_prev;
+        f[6] = (double)t / T;
+        f[7] = l.acc;
+        forced = 0;
+        if (p.policy == DIT_POLICY_GATE) {
+          z = gate_logit(gate, f);
+          dec = (z > thr) ? 1 : 0;
+          if (B - l.cnt >= T - t) { dec = 1; forced = 1; }
+          if (B - l.cnt == 0) { dec = 0; forced = 1; }
+        } else if (p.policy == DIT_POLICY_STATIC) {
+          dec = mu[t];
+        } else {
+          z = l.acc;
+          dec = (l.acc > p.delta) ? 1 : 0;
         }
-      const double d_prev = sums[0] / std::max(sums[1], 1e-30);
-      const double d_last = sums[2] / std::max(sums[3], 1e-30);
-      acc += d_prev;
-      f[0] = (double)B / T;
-      f[1] = (double)(B - cnt) / B;
-      f[2] = (double)(B - cnt) / (T - t);
-      f[3] = (double)(t - t_last);
-      f[4] = d_last;
-      f[5] = d_prev;
-      f[6] = (double)t / T;
-      f[7] = acc;
-      forced = 0;
-      if (p.policy == DIT_POLICY_GATE) {
-        z = gate_logit(gate, f);
-        dec = (z > thr) ? 1 : 0;
-        if (B - cnt >= T - t) { dec = 1; forced = 1; }
-        if (B - cnt == 0) { dec = 0; forced = 1; }
-      } else if (p.policy == DIT_POLICY_STATIC) {
-        dec = mu[t];
-      } else {
-        z = acc;
-        dec = (acc > p.delta) ? 1 : 0;
+        if (p.forced_mask) dec = p.forced_mask[(size_t)j * T + t] ? 1 : 0;
       }
-      if (p.forced_mask) dec = p.forced_mask[t] ? 1 : 0;
+      l.dec = dec != 0;
+      if (l.dec) comp.push_back(j);
+      dit_schedule& o = out[j];
+      o.full[t] = (uint8_t)dec;
+      if (o.logit) o.logit[t] = (float)z;
+      if (o.forced) o.forced[t] = (uint8_t)forced;
+      if (o.features)
+        for (int k = 0; k < DIT_N_FEATURES; ++k) o.features[(size_t)t * DIT_N_FEATURES + k] = f[k];
+      if (o.sums)
+        for (int k = 0; k < 4; ++k) o.sums[(size_t)t * 4 + k] = sums[k];
+    }
+    if (t > 0)
       c->stats.host_gate_ms +=
           std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - h0).count();
-    }
-    out->full[t] = (uint8_t)dec;
-    if (out->logit) out->logit[t] = (float)z;
-    if (out->forced) out->forced[t] = (uint8_t)forced;
-    if (out->features)
-      for (int k = 0; k < DIT_N_FEATURES; ++k) out->features[(size_t)t * DIT_N_FEATURES + k] = f[k];
-    if (out->sums)
-      for (int k = 0; k < 4; ++k) out->sums[(size_t)t * 4 + k] = sums[k];
 
-    // (a4) full or reuse, (a5) final layer + step rule
-    const float dsig = (float)(sig[t + 1] - sig[t]);
-    const bool unipc = p.solver == DIT_SOLVER_UNIPC;
-    if (fused && !dec) {
-      // h + r, final adaLN, projection, guidance and Euler in one pass per row tile
-      Scope sc(c, DIT_K_REUSE, (double)c->nb * N * H * c->esz);
-      const float* mf0 = s.modp[0] + (c->n_mod - 2 * H);
-      const float* mf1 = pair ? s.modp[1] + (c->n_mod - 2 * H) : nullptr;
-      HIPCK(dit::launch_reuse_final(latent, c->C, c->M.img_in.w, c->M.img_in.b, c->r, c->nb, c->M.fin.w,
-                                    c->M.fin.b, mf0, mf1, dsig, (float)p.guidance, N, H,
-                                    unipc ? c->vel : nullptr, c->stream));
-    } else {
-      if (fused) {  // the block stack's input h, bit-identical to the one the indicator used
-        Scope sc(c, DIT_K_FULL_OTHER, (double)N * H * c->esz);
-        HIPCK(dit::launch_reuse_indicator(latent, c->C, c->M.img_in.w, c->M.img_in.b, nullptr, nullptr, nullptr,
-                                          N, H, nullptr, nullptr, nullptr, nullptr, c->h, c->stream));
+    // the step rule of sample j once its velocity (or velocities) are in vel
+    auto step_rule = [&](int j, bool vpair, bool folded) -> dit_status {
+      Lane& l = c->lanes[j];
+      if (!unipc && folded) return DIT_OK;
+      Scope sc(c, l.dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
+      if (unipc) {
+        // the guidance pair's two velocities are combined here unless the
+        // fused reuse kernel has already combined them
+        const dit::UniCoef k = unipc_coef(sig, t, T);
+        float* m_t = l.mh[t % 3];
+        const float* m_s = t >= 1 ? l.mh[(t + 2) % 3] : nullptr;
+        const float* m_p = (t >= 2 && k.cp != 0.f) ? l.mh[(t + 1) % 3] : nullptr;
+        HIPCK(dit::launch_unipc(lat(j), c->vel, vpair ? c->vel + NC : nullptr, (float)p.guidance, (float)sig[t],
+                                l.x_last, (k.pp != 0.f || k.corr) ? m_s : nullptr, m_p, m_t, k, (int64_t)NC,
+                                c->stream));
+      } else if (!folded) {
+        HIPCK(dit::launch_euler(lat(j), c->vel, pair ? c->vel + NC : nullptr, (float)p.guidance, dsig,
+                                (int64_t)NC, c->stream));
       }
-      const bool fused_euler = !pair && proj_fits(c) && !unipc;
-      float* lat_f = fused_euler ? latent : nullptr;
-      if (dec && c->pair_batched) TRY(full_stack_pair(c, s));
-      for (int b = 0; b < c->nb; ++b) {
-        if (dec) {
+      return DIT_OK;
+    };
+
+    // (a4) reuse, (a5) final layer + step rule, sample by sample
+    for (int j = 0; j < S; ++j) {
+      Lane& l = c->lanes[j];
+      if (l.dec) continue;
+      if (fused) {
+        // h + r, final adaLN, projection, guidance and Euler in one pass per row tile
+        Scope sc(c, DIT_K_REUSE, (double)nb * NH * c->esz);
+        const float* mf0 = modp(j, 0, t) + (c->n_mod - 2 * H);
+        const float* mf1 = pair ? modp(j, 1, t) + (c->n_mod - 2 * H) : nullptr;
+        HIPCK(dit::launch_reuse_final(lat(j), C, c->M.img_in.w, c->M.img_in.b, l.r, nb, c->M.fin.w, c->M.fin.b,
+                                      mf0, mf1, dsig, (float)p.guidance, N, H, unipc ? c->vel : nullptr,
+                                      c->stream));
+        if (unipc) TRY(step_rule(j, false, true));
+        continue;
+      }
+      for (int b = 0; b < nb; ++b) {
+        {
+          // h_out = S(h + r) and the final adaLN in one pass over the rows
+          Scope sc(c, DIT_K_REUSE, 3.0 * NH * c->esz);
+          const float* mf = modp(j, b, t) + (c->n_mod - 2 * H);
+          TRY(typed(c, [&](auto* tp) {
+            using Ty = std::remove_pointer_t<decltype(tp)>;
+            return dit::launch_add_ln_mod<Ty>((const Ty*)l.h, (const Ty*)sp(c, l.r, b * NH), (Ty*)c->yf, N, H, mf,
+                                              mf + H, c->stream);
+          }));
+        }
+        TRY(final_project(c, b, DIT_K_REUSE, fused_euler ? lat(j) : nullptr, dsig));
+      }
+      TRY(step_rule(j, pair, fused_euler));
+    }
+
+    // (a4) full: the computing samples' block stacks, (a5) per sample
+    if (!comp.empty()) {
+      if (fused)  // the block stack's input h, bit-identical to the one the indicator used
+        for (int j : comp) {
+          Scope sc(c, DIT_K_FULL_OTHER, (double)NH * c->esz);
+          HIPCK(dit::launch_reuse_indicator(lat(j), C, c->M.img_in.w, c->M.img_in.b, nullptr, nullptr, nullptr, N,
+                                            H, nullptr, nullptr, nullptr, nullptr, c->lanes[j].h, c->stream));
+        }
+      seqs.clear();
+      for (int j : comp)
+        for (int b = 0; b < nb; ++b) {
+          Lane& l = c->lanes[j];
+          seqs.push_back(Seq{sp(c, l.txt, (size_t)b * c->Nt * H), l.h, sp(c, l.r, b * NH), modp(j, b, t),
+                             modxp(j, b)});
+        }
+      const int Q = (int)seqs.size();
+      if (c->stacked) TRY(full_stack_multi(c, seqs.data(), Q));
+      for (size_t k = 0; k < comp.size(); ++k) {
+        const int j = comp[k];
+        for (int b = 0; b < nb; ++b) {
+          const int q = (int)k * nb + b;
           const void* hout;
-          if (c->pair_batched) {
-            hout = sp(c, c->X, (size_t)c->nb * c->Nt * H + (size_t)b * N * H);
+          if (c->stacked) {
+            hout = sp(c, c->X, ((size_t)Q * c->Nt + (size_t)q * N) * H);
           } else {
-            TRY(full_stack(c, b, s));
+            TRY(full_stack(c, seqs[q], t, T));
             hout = c->cfg.n_cross ? c->X : sp(c, c->X, (size_t)c->Nt * H);
           }
-          TRY(final_layer(c, b, hout, s, DIT_K_FULL_OTHER, lat_f, dsig));
-        } else {
-          {
-            // h_out = S(h + r) and the final adaLN in one pass over the rows
-            Scope sc(c, DIT_K_REUSE, 3.0 * N * H * c->esz);
-            const float* mf = s.modp[b] + (c->n_mod - 2 * H);
-            TRY(typed(c, [&](auto* tp) {
-              using Ty = std::remove_pointer_t<decltype(tp)>;
-              return dit::launch_add_ln_mod<Ty>((const Ty*)c->h, (const Ty*)sp(c, c->r, (size_t)b * N * H),
-                                                (Ty*)c->yf, N, H, mf, mf + H, c->stream);
-            }));
-          }
-          TRY(final_project(c, b, DIT_K_REUSE, lat_f, dsig));
+          TRY(final_layer(c, b, hout, seqs[q].mod, DIT_K_FULL_OTHER, fused_euler ? lat(j) : nullptr, dsig));
         }
-      }
-      if (!fused_euler && !unipc) {
-        Scope sc(c, dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
-        HIPCK(dit::launch_euler(latent, c->vel, pair ? c->vel + (size_t)N * c->C : nullptr,
-                                (float)p.guidance, dsig, (int64_t)N * c->C, c->stream));
+        TRY(step_rule(j, pair, fused_euler));
       }
     }
-    if (unipc) {
-      // the guidance pair's two velocities are combined here; the fused reuse
-      // kernel has already combined them
-      const bool vpair = pair && !(fused && !dec);
-      const dit::UniCoef k = unipc_coef(sig, t, T);
-      float* m_t = c->mh[t % 3];
-      const float* m_s = t >= 1 ? c->mh[(t + 2) % 3] : nullptr;
-      const float* m_p = (t >= 2 && k.cp != 0.f) ? c->mh[(t + 1) % 3] : nullptr;
-      Scope sc(c, dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
-      HIPCK(dit::launch_unipc(latent, c->vel, vpair ? c->vel + (size_t)N * c->C : nullptr, (float)p.guidance,
-                              (float)sig[t], c->x_last, (k.pp != 0.f || k.corr) ? m_s : nullptr, m_p, m_t, k,
-                              (int64_t)N * c->C, c->stream));
+
+    for (int j = 0; j < S; ++j) {
+      Lane& l = c->lanes[j];
+      if (l.dec) {
+        l.cnt += 1;
+        l.t_last = t;
+        l.acc = 0.0;
+        l.i_last = l.i_new;
+        c->stats.full_steps += 1;
+      } else {
+        c->stats.reuse_steps += 1;
+      }
+      l.i_prev = l.i_new;
+      out[j].nfe = l.cnt;
+      out[j].steps_done = t + 1;
     }
-    if (dec) {
-      cnt += 1;
-      t_last = t;
-      acc = 0.0;
-      i_last = i_new;
-      c->stats.full_steps += 1;
-    } else {
-      c->stats.reuse_steps += 1;
-    }
-    i_prev = i_new;
-    out->nfe = cnt;
-    out->steps_done = t + 1;
   }
   HIPCK(hipStreamSynchronize(c->stream));
-  if (cnt != B && p.policy != DIT_POLICY_THRESHOLD)
-    return fail(c, DIT_EBUDGET, "realised NFE differs from the budget");
+  if (p.policy != DIT_POLICY_THRESHOLD)
+    for (int j = 0; j < S; ++j)
+      if (c->lanes[j].cnt != B)
+        return fail(c, DIT_EBUDGET, "realised NFE differs from the budget (sample " + std::to_string(j) + ")");
   return DIT_OK;
 }
 
@@ -1115,7 +1297,7 @@ dit_status dit_cache_create(const dit_model_config* cfg, const void* weights, si
   c->H = cfg->hidden; c->F = cfg->mlp_hidden; c->N = cfg->n_img; c->Nt = cfg->n_txt;
   c->L = cfg->n_cross ? cfg->n_img : cfg->n_img + cfg->n_txt;
   c->C = cfg->in_channels; c->nb = cfg->batch;
-  c->pair_batched = c->bf16 && c->nb == 2 && !cfg->pooled_text && !cfg->n_cross;
+  c->stacked = c->bf16 && !cfg->n_cross;
   c->n_mod = 12 * c->H * cfg->n_double + 3 * c->H * cfg->n_single + (cfg->n_cross ? 6 * c->H : 0) + 2 * c->H;
   c->ldY = 4 * c->H + c->F;
   int dev = 0;
@@ -1149,13 +1331,18 @@ dit_status dit_cache_create(const dit_model_config* cfg, const void* weights, si
   return DIT_OK;
 }
 
-dit_status dit_cache_sample_ex(dit_cache* c, float* latent, const void* text_emb, const float* gate_weights,
-                               size_t gate_len, const dit_sample_params* p, dit_schedule* out) {
+dit_status dit_cache_sample_batch(dit_cache* c, int32_t n_samples, float* latents, const void* text_emb,
+                                  const float* gate_weights, size_t gate_len, const dit_sample_params* p,
+                                  dit_schedule* out) {
   if (!c) return DIT_EINVAL;
   c->err.clear();
-  if (!latent || !text_emb || !p || !out || !out->full) return fail(c, DIT_EINVAL, "null argument");
-  out->nfe = 0;
-  out->steps_done = 0;
+  if (!latents || !text_emb || !p || !out) return fail(c, DIT_EINVAL, "null argument");
+  if (n_samples < 1) return fail(c, DIT_EINVAL, "need n_samples >= 1");
+  for (int j = 0; j < n_samples; ++j) {
+    if (!out[j].full) return fail(c, DIT_EINVAL, "null schedule array");
+    out[j].nfe = 0;
+    out[j].steps_done = 0;
+  }
   if (p->T < 1 || p->B < 1 || p->B > p->T) return fail(c, DIT_EBUDGET, "need 1 <= B <= T");
   if (!(p->tau > 0.0 && p->tau < 1.0)) return fail(c, DIT_EINVAL, "tau must be in (0, 1)");
   if (p->indicator != DIT_INDICATOR_MODULATED && p->indicator != DIT_INDICATOR_PATCH)
@@ -1166,25 +1353,32 @@ dit_status dit_cache_sample_ex(dit_cache* c, float* latent, const void* text_emb
   if (p->solver != DIT_SOLVER_EULER && p->solver != DIT_SOLVER_UNIPC) return fail(c, DIT_EINVAL, "bad solver");
   if (p->policy == DIT_POLICY_THRESHOLD && std::isnan(p->delta))
     return fail(c, DIT_EINVAL, "threshold delta is NaN");
-  if (p->forced_mask) {
-    int ones = 0;
-    for (int t = 0; t < p->T; ++t) {
-      if (p->forced_mask[t] > 1) return fail(c, DIT_EINVAL, "forced mask entries must be 0/1");
-      ones += p->forced_mask[t];
+  if (p->forced_mask)
+    for (int j = 0; j < n_samples; ++j) {
+      const uint8_t* fm = p->forced_mask + (size_t)j * p->T;
+      int ones = 0;
+      for (int t = 0; t < p->T; ++t) {
+        if (fm[t] > 1) return fail(c, DIT_EINVAL, "forced mask entries must be 0/1");
+        ones += fm[t];
+      }
+      if (fm[0] != 1) return fail(c, DIT_EINVAL, "forced mask needs m_0 = 1");
+      if (p->policy != DIT_POLICY_THRESHOLD && ones != p->B)
+        return fail(c, DIT_EINVAL, "forced mask needs exactly B ones");
     }
-    if (p->forced_mask[0] != 1) return fail(c, DIT_EINVAL, "forced mask needs m_0 = 1");
-    if (p->policy != DIT_POLICY_THRESHOLD && ones != p->B)
-      return fail(c, DIT_EINVAL, "forced mask needs exactly B ones");
-  }
   GateMLP gate;
   if (p->policy == DIT_POLICY_GATE) TRY(parse_gate(c, gate_weights, gate_len, gate));
   const auto t0 = std::chrono::steady_clock::now();
-  dit_status st = run_sample(c, latent, text_emb, gate, *p, out);
+  dit_status st = run_batch(c, n_samples, latents, text_emb, gate, *p, out);
   if (st != DIT_OK) hipStreamSynchronize(c->stream);
   collect_events(c);
   c->stats.sample_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
-  c->stats.samples += (st == DIT_OK);
+  c->stats.samples += (st == DIT_OK) ? n_samples : 0;
   return st;
+}
+
+dit_status dit_cache_sample_ex(dit_cache* c, float* latent, const void* text_emb, const float* gate_weights,
+                               size_t gate_len, const dit_sample_params* p, dit_schedule* out) {
+  return dit_cache_sample_batch(c, 1, latent, text_emb, gate_weights, gate_len, p, out);
 }
 
 dit_status dit_cache_sample(dit_cache* c, float* latent, const void* text_emb, int32_t T, int32_t B,
@@ -1199,10 +1393,10 @@ dit_status dit_cache_sample(dit_cache* c, float* latent, const void* text_emb, i
 void dit_cache_destroy(dit_cache* c) {
   if (!c) return;
   if (c->stream) hipStreamSynchronize(c->stream);
-  free_per_sample(c);
-  void* ps[] = {c->wdev, c->xs, c->h, c->mbuf[0], c->mbuf[1], c->mbuf[2], c->r, c->X, c->A, c->Y, c->vt,
-                c->yf, c->vel, c->txt, c->ctxkv, c->vt2, c->ones, c->partials, c->x_last, c->mh[0],
-                c->mh[1], c->mh[2]};
+  free_per_call(c);
+  for (Lane& l : c->lanes) free_lane(l);
+  void* ps[] = {c->wdev, c->xs, c->X, c->A, c->Y, c->vt, c->modq, c->yf, c->vel, c->ctxkv, c->vt2, c->ones,
+                c->partials};
   for (void* p : ps)
     if (p) hipFree(p);
   if (c->sums_host) hipHostFree(c->sums_host);

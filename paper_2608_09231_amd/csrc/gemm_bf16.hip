@@ -30,8 +30,9 @@ struct Prob {
   const bf16_t* bias;
   void* C; int64_t ldc;
   const float* gate;
+  int64_t gstride;  // gate vector of row m: gate + (m / gseg) * gstride (gseg > 0)
   int M, N, K;
-  int flags, rms_cols, gelu_from, gap_at, gap;
+  int flags, rms_cols, gelu_from, gap_at, gap, gseg;
   int tiles_m, tiles_n;
 };
 
@@ -127,7 +128,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(Batch b) {
   if ((int)blockIdx.x >= b.total) return;
   int lt = xcd_remap(blockIdx.x, b.total);
   const bool second = lt >= b.tiles0;
-  const Prob P = second ? b.p1 : b.p0;
+  Prob P = second ? b.p1 : b.p0;
   if (second) lt -= b.tiles0;
 
   // M-grouped tile order (8 tile-rows per group).
@@ -139,6 +140,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(Batch b) {
   const int tm = first_m + (lt % in_group) % gsz;
   const int tn = (lt % in_group) / gsz;
   const int m0 = tm * BM, n0 = tn * BN;
+  // per-segment gate vectors: the host admits only BM | gseg, so a tile's
+  // rows share one vector
+  if (P.gseg > 0) P.gate += (int64_t)(m0 / P.gseg) * P.gstride;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -425,7 +429,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
   if ((int)blockIdx.x >= b.total) return;
   int lt = xcd_remap(blockIdx.x, b.total);
   const bool second = lt >= b.tiles0;
-  const Prob P = second ? b.p1 : b.p0;
+  Prob P = second ? b.p1 : b.p0;
   if (second) lt -= b.tiles0;
   constexpr int GROUP = 8;
   const int in_group = GROUP * P.tiles_n;
@@ -435,6 +439,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
   const int tm = first_m + (lt % in_group) % gsz;
   const int tn = (lt % in_group) / gsz;
   const int m0 = tm * BM, n0 = tn * BN;
+  // per-segment gate vectors: the host admits only BM | gseg, so a tile's
+  // rows share one vector
+  if (P.gseg > 0) P.gate += (int64_t)(m0 / P.gseg) * P.gstride;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -675,6 +682,7 @@ Prob make_prob(const GemmArgs& g, int bm, int bn) {
   p.bias = (const bf16_t*)g.bias;
   p.C = g.C; p.ldc = g.ldc;
   p.gate = g.gate;
+  p.gseg = g.gseg; p.gstride = g.gstride;
   p.M = g.M; p.N = g.N; p.K = g.K;
   p.flags = g.flags; p.rms_cols = g.rms_cols;
   p.gelu_from = g.gelu_from; p.gap_at = g.gap_at; p.gap = g.gap;
@@ -710,6 +718,8 @@ int pick_cfg(const GemmArgs* g, int n, int n_cu) {
   }
   auto admits = [&](const Cfg& k) {
     if (rms && k.wn % 128) return false;
+    for (int i = 0; i < n; ++i)
+      if (g[i].gseg > 0 && g[i].gseg % k.bm) return false;
     if (!k.dma) return true;
     if (!aligned || !off32 || (k.lds_epi && !epi_ok)) return false;
     for (int i = 0; i < n; ++i)
@@ -762,7 +772,11 @@ hipError_t launch_proj_small_n(const void* A, int64_t lda, const void* W, int64_
 
 hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t stream, int n_cu) {
   if (n < 1 || n > 2) return hipErrorInvalidValue;
+  for (int i = 0; i < n; ++i)
+    if (g[i].gseg < 0 || (g[i].gseg > 0 && (g[i].gseg % 32 || !(g[i].flags & DIT_EPI_GATED_RES))))
+      return hipErrorInvalidValue;
   const int c = pick_cfg(g, n, n_cu);
+  if (c < 0) return hipErrorInvalidValue;
   const Cfg& k = kCfgs[c];
   Batch b;
   b.p0 = make_prob(g[0], k.bm, k.bn);

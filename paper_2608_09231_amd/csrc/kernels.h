@@ -20,9 +20,14 @@ struct GemmArgs {
   int gelu_from = 0x7fffffff;
   int gap_at = 0x7fffffff;
   int gap = 0;
+  // Gated residual with one gate vector per segment of gseg rows: row m uses
+  // gate + (m / gseg) * gstride.  gseg = 0: one vector; else a multiple of 32.
+  int gseg = 0;
+  int64_t gstride = 0;
 };
 
-// bf16 MFMA GEMM; n = 1 or 2 independent problems in one launch.
+// bf16 MFMA GEMM; n = 1 or 2 independent problems in one launch.  Invalid
+// arguments (no tile configuration admits the problem) return an error.
 hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t s, int n_cu);
 // v = A W^T + bias for N <= 128 (multiple of 16), K % 32 == 0, f32 output; with
 // x != nullptr the result goes into the Euler update x += alpha * v instead.
@@ -35,13 +40,18 @@ hipError_t launch_gemm_f32(const GemmArgs* g, int n, hipStream_t s);
 // Flash attention, bf16, head_dim 128. vt = v transposed per head:
 // [heads][128][ldvt], ldvt = round_up(Lk, 64), zero padded.  Rows r >= split
 // of q, k, v and o are stored gap rows further down (a joint sequence split
-// over a branch-batched buffer); split = INT_MAX for one contiguous piece.
+// over a buffer of stacked sequences); split = INT_MAX for one contiguous
+// piece.  nseq independent sequences in one launch: sequence z's rows start
+// z * zs rows down, its gap is gap + z * gz, its vt block is the z-th
+// [heads][128][ldvt] block.
 hipError_t launch_transpose_v_bf16(const void* v, int64_t ldv, void* vt, int Lk, int heads,
-                                   hipStream_t s, int split = 0x7fffffff, int64_t gap = 0);
+                                   hipStream_t s, int split = 0x7fffffff, int64_t gap = 0, int nseq = 1,
+                                   int64_t zs = 0, int64_t gz = 0);
 hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int64_t ldk,
                                   const void* vt, int ldvt, void* o, int64_t ldo, int Lq,
                                   int Lk, int heads, bool bounded_logits, hipStream_t s,
-                                  int split = 0x7fffffff, int64_t gap = 0);
+                                  int split = 0x7fffffff, int64_t gap = 0, int nseq = 1, int64_t zs = 0,
+                                  int64_t gz = 0);
 // f32 attention, head_dim <= 128 (multiple of 4).
 hipError_t launch_attn_f32(const float* q, int64_t ldq, const float* k, int64_t ldk,
                            const float* v, int64_t ldv, float* o, int64_t ldo, int Lq, int Lk,
@@ -50,10 +60,12 @@ hipError_t launch_attn_f32(const float* q, int64_t ldq, const float* k, int64_t 
 // ---- streaming kernels, templated on the storage type (float or bf16) ----
 // out = S(LN(x) * (1 + scale) + shift) per row; rows < split use (sh0, sc0),
 // the others (sh1, sc1); mod vectors are f32.  scale == nullptr: plain LN.
+// Several sequences stacked by rows: row r < split takes its vectors
+// (r / seg0) * mstride floats further on, row r >= split (r - split) / seg1.
 template <typename T>
 hipError_t launch_ln_mod(const T* x, int64_t ldx, T* out, int64_t ldo, int rows, int H, int split,
                          const float* sh0, const float* sc0, const float* sh1, const float* sc1,
-                         hipStream_t s);
+                         hipStream_t s, int seg0 = 0x7fffffff, int seg1 = 0x7fffffff, int64_t mstride = 0);
 // Indicator: m = S(LN(h)(1+sc)+sh) (or m = h when sc == nullptr), written
 // to m_out; with partials != nullptr the relative-L1 sums |m-mp|, |mp|,
 // |m-ml|, |ml| are reduced in a fixed order into out[4] (f64, host-mapped)

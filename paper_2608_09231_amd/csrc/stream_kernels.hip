@@ -112,7 +112,8 @@ template <typename T, int MAXC, bool FULL>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, int64_t ldx,
                                                     T* __restrict__ out, int64_t ldo, int rows, int H,
                                                     int split, const float* sh0, const float* sc0,
-                                                    const float* sh1, const float* sc1) {
+                                                    const float* sh1, const float* sc1, int seg0, int seg1,
+                                                    int64_t mstride) {
   constexpr int E = Chunk<T>::E;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -121,8 +122,11 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, in
   r.load(x + (int64_t)row * ldx, H, lane);
   float mean, rstd;
   r.stats(H, lane, mean, rstd);
-  const float* sh = row < split ? sh0 : sh1;
-  const float* sc = row < split ? sc0 : sc1;
+  const bool lo = row < split;
+  const int64_t mo = (int64_t)(lo ? row / seg0 : (row - split) / seg1) * mstride;
+  const float* sh = (lo ? sh0 : sh1) + mo;
+  const float* sc = lo ? sc0 : sc1;
+  if (sc) sc += mo;
   T* o = out + (int64_t)row * ldo;
   if (sc) {
 #pragma unroll
@@ -438,12 +442,12 @@ hipError_t dispatch_maxc(int H, F f) {
 template <typename T>
 hipError_t launch_ln_mod(const T* x, int64_t ldx, T* out, int64_t ldo, int rows, int H, int split,
                          const float* sh0, const float* sc0, const float* sh1, const float* sc1,
-                         hipStream_t s) {
-  if (H % Chunk<T>::E) return hipErrorInvalidValue;
+                         hipStream_t s, int seg0, int seg1, int64_t mstride) {
+  if (H % Chunk<T>::E || seg0 < 1 || seg1 < 1) return hipErrorInvalidValue;
   if (rows <= 0) return hipSuccess;
   return dispatch_maxc<T>(H, [&](auto mc, auto fl) {
     hipLaunchKernelGGL((ln_mod_kernel<T, decltype(mc)::value, decltype(fl)::value>), dim3((rows + 3) / 4), dim3(256), 0, s, x,
-                       ldx, out, ldo, rows, H, split, sh0, sc0, sh1, sc1);
+                       ldx, out, ldo, rows, H, split, sh0, sc0, sh1, sc1, seg0, seg1, mstride);
     return hipGetLastError();
   });
 }
@@ -549,7 +553,8 @@ hipError_t launch_add_offset(const float* mod, int64_t ld, int base, const T* of
 
 #define DIT_INST(T)                                                                              \
   template hipError_t launch_ln_mod<T>(const T*, int64_t, T*, int64_t, int, int, int, const float*, \
-                                       const float*, const float*, const float*, hipStream_t);     \
+                                       const float*, const float*, const float*, hipStream_t, int, \
+                                       int, int64_t);                                              \
   template hipError_t launch_indicator<T>(const T*, T*, const T*, const T*, int, int, const float*, \
                                           const float*, double*, double*, hipStream_t);            \
   template hipError_t launch_add_ln_mod<T>(const T*, const T*, T*, int, int, const float*, const float*, \

@@ -142,6 +142,14 @@ WORKLOADS = {
            hidden=256, heads=2, head_dim=128, mlp_hidden=1024, in_channels=64,
            ctx_dim=72, n_img=136, n_txt=24, batch=2, pooled_text=False),
         T=8, B=4, shift=3.0, guidance=4.0, seed=5),
+    # Token counts that are multiples of 32: the stacked block stack gates
+    # the residual of each sequence inside one GEMM launch.
+    "small_seg_bf16": Workload(
+        "small_seg_bf16",
+        _m(name="small_seg_bf16", dtype="bf16", n_double=2, n_single=2, n_cross=0,
+           hidden=256, heads=2, head_dim=128, mlp_hidden=1024, in_channels=64,
+           ctx_dim=96, n_img=512, n_txt=128),
+        T=8, B=4, shift=3.0, guidance=1.0, seed=13),
     "small_cross_bf16": Workload(
         "small_cross_bf16",
         _m(name="small_cross_bf16", dtype="bf16", n_double=0, n_single=0, n_cross=2,

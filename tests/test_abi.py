@@ -62,6 +62,7 @@ def test_null_arguments():
     lib = binding.load()
     assert lib.dit_cache_create(None, None, 0, None, None) == binding.DIT_EINVAL
     assert lib.dit_cache_sample(None, None, None, 1, 1, None, 0, None) == binding.DIT_EINVAL
+    assert lib.dit_cache_sample_batch(None, 2, None, None, None, 0, None, None) == binding.DIT_EINVAL
     assert lib.dit_cache_set_profiling(None, 1) == binding.DIT_EINVAL
     assert lib.dit_gemm_bf16(None, None) == binding.DIT_EINVAL
 
