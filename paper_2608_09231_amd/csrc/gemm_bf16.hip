@@ -2,14 +2,16 @@
 // epilogues of the DiT blocks:  C = epi(A . W^T + bias).
 //
 // A [M,K] and W [N,K] are both K-contiguous (W in nn.Linear [out,in]
-// layout), so every MFMA operand is a 16-byte run of K.  Tiles of BM x BN
-// are staged through LDS in BK = 64 slices, double-buffered, with the
-// 16-byte chunks of each 128-byte row XOR-swizzled by ((row >> 1) & 7): two
-// consecutive 128-byte rows fill one 256-byte bank cycle, so the fragment
-// reads of 16 consecutive rows hit 16 distinct 16-byte bank groups.  Four waves
-// per workgroup, each owning a WM x WN sub-tile of 32x32 MFMA tiles.
-// Workgroups are remapped so that each of the 8 XCDs walks a contiguous,
-// M-grouped range of tiles (its own L2 sees the shared A rows / W columns).
+// layout), so every MFMA operand is a 16-byte run of K.  Tiles are staged
+// through LDS in BK = 64 slices (128-byte rows) by buffer loads with an LDS
+// destination, the 16-byte chunks of each row XOR-swizzled by
+// ((row >> 1) & 7): two consecutive 128-byte rows fill one 256-byte bank
+// cycle, so the fragment reads of 16 consecutive rows hit 16 distinct 16-byte
+// bank groups.  The main kernel (256 x 256 tiles, 8 waves of 64 x 128) keeps
+// a ring of five operand slices in LDS so A slices arrive two slices ahead;
+// smaller tiles use a two-stage pipeline.  Workgroups are remapped so that
+// each of the 8 XCDs walks a contiguous, M-grouped range of tiles (its own L2
+// sees the shared A rows / W columns).
 #include <stdlib.h>
 
 #include <type_traits>
@@ -597,6 +599,170 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
   }
 }
 
+// vmcnt(N) and lgkmcnt(0) in one wait (same encoding as wait_vmcnt).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | ((N >> 4) << 14));
+}
+
+// Workgroup barrier without the workgroup-scope fence of __syncthreads: that
+// fence waits for every outstanding global load of the wave, copies to LDS
+// included, which would drain the copies a deeper pipeline keeps in flight.
+// The memory clobber keeps the compiler from moving memory operations across
+// it; callers wait for their own LDS reads and copies first.
+__device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
+
+// 256 x 256 tiles, 8 waves of 64 x 128, BK = 64, with the whole 160 KB of
+// LDS as a ring of five 32 KB operand slices: operand i (A slice s = 2s,
+// W slice s = 2s + 1) lives in unit i % 5.  When slice kt starts, the units
+// of slice kt-1 are free and receive W slice kt+1 and A slice kt+2, so A
+// slices are copied two slices ahead of use and W slices one ahead, and the
+// end-of-slice wait leaves the A copies in flight.  The substep schedule is
+// the one of the two-stage kernel above (fragments double-buffered in
+// registers, LDS reads of the next substep between the MFMAs).
+// Requires K % 64 == 0, K >= 128 and the LDS-staged epilogue's conditions.
+__global__ __launch_bounds__(512) void gemm_bf16_ring_kernel(Batch b) {
+  constexpr int BM = 256, BN = 256, BK_ = 64, WGN = 2;
+  constexpr int WM = 64, WN = 128, TM = 2, TN = 4;
+  constexpr int UNIT = 256 * BK_ * 2;  // one operand slice
+  constexpr int INS = 4;                // 1 KB copies per wave per operand slice
+  __shared__ __attribute__((aligned(1024))) char smem[5 * UNIT];
+
+  if ((int)blockIdx.x >= b.total) return;
+  int lt = xcd_remap(blockIdx.x, b.total);
+  const bool second = lt >= b.tiles0;
+  Prob P = second ? b.p1 : b.p0;
+  if (second) lt -= b.tiles0;
+  constexpr int GROUP = 8;
+  const int in_group = GROUP * P.tiles_n;
+  const int gid = lt / in_group;
+  const int first_m = gid * GROUP;
+  const int gsz = min(P.tiles_m - first_m, GROUP);
+  const int tm = first_m + (lt % in_group) % gsz;
+  const int tn = (lt % in_group) / gsz;
+  const int m0 = tm * BM, n0 = tn * BN;
+  // per-segment gate vectors: the host admits only BM | gseg
+  if (P.gseg > 0) P.gate += (int64_t)(m0 / P.gseg) * P.gstride;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int lrow = lane & 31, lhalf = lane >> 5;
+
+  // per-lane source byte offsets: copy j of this wave moves rows
+  // 8 (4 wave + j) .. + 7 of the slice, 16-byte chunks XOR-swizzled by
+  // ((row >> 1) & 7) as in the two-stage kernel
+  uint32_t aoff[INS], boff[INS];
+#pragma unroll
+  for (int j = 0; j < INS; ++j) {
+    const int row = 8 * (wave * INS + j) + (lane >> 3);
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    aoff[j] = ((uint32_t)min(m0 + row, P.M - 1) * (uint32_t)P.lda + c * 8) * 2u;
+    boff[j] = ((uint32_t)min(n0 + row, P.N - 1) * (uint32_t)P.ldw + c * 8) * 2u;
+  }
+  auto unit = [&](int op) { return smem + (op % 5) * UNIT; };
+  auto issue_a = [&](int s) {
+    char* d = unit(2 * s);
+    const uint32_t so = (uint32_t)s * BK_ * 2;
+#pragma unroll
+    for (int j = 0; j < INS; ++j) buf_lds16(P.A, (lds_void_t*)(d + (wave * INS + j) * 1024), aoff[j], so);
+  };
+  auto issue_w = [&](int s) {
+    char* d = unit(2 * s + 1);
+    const uint32_t so = (uint32_t)s * BK_ * 2;
+#pragma unroll
+    for (int j = 0; j < INS; ++j) buf_lds16(P.W, (lds_void_t*)(d + (wave * INS + j) * 1024), boff[j], so);
+  };
+  auto rd = [&](int kt, int s, bf16x8_t(&af)[TM], bf16x8_t(&bfr)[TN]) {
+    const char* sA = unit(2 * kt);
+    const char* sB = unit(2 * kt + 1);
+    const int kc = 2 * s + lhalf;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int row = wm * WM + i * 32 + lrow;
+      af[i] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sA + row * 128 + ((kc ^ ((row >> 1) & 7)) << 4)));
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int row = wn * WN + j * 32 + lrow;
+      bfr[j] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sB + row * 128 + ((kc ^ ((row >> 1) & 7)) << 4)));
+    }
+  };
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  EpiLds epi(P, m0 + wm * WM, n0 + wn * WN, lrow, lhalf, (float*)smem + wave * (32 * 128));
+  epi.prep();
+  auto mm = [&](const bf16x8_t(&af)[TM], const bf16x8_t(&bfr)[TN]) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+  };
+  // one MFMA, then the copies of this substep (if any) and two LDS reads,
+  // three times; then the other five MFMAs; a fence closes the substep
+  auto sched = [&](auto with_copy) {
+    constexpr bool WithCopy = decltype(with_copy)::value;
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      if constexpr (WithCopy) __builtin_amdgcn_sched_group_barrier(0x010, 2, 0);  // VMEM
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - 3, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  using copy_t = std::integral_constant<bool, true>;
+  using nocopy_t = std::integral_constant<bool, false>;
+
+  const int nk = P.K / BK_;  // >= 2
+  bf16x8_t a0[TM], b0[TN], a1[TM], b1[TN];
+  issue_a(0);
+  issue_w(0);
+  issue_a(1);
+  wait_vmcnt_lgkm0<INS>();  // slice 0 has landed; A slice 1 may be in flight
+  barrier_no_fence();
+  rd(0, 0, a0, b0);
+  // slice kt with W slice kt+1 (HW) and A slice kt+2 (HA) copied meanwhile
+  auto slice = [&](int kt, auto hw, auto ha) {
+    constexpr bool HW = decltype(hw)::value, HA = decltype(ha)::value;
+    if constexpr (HW) issue_w(kt + 1);
+    rd(kt, 1, a1, b1); mm(a0, b0);
+    if constexpr (HW) sched(copy_t{}); else sched(nocopy_t{});
+    if constexpr (HA) issue_a(kt + 2);
+    rd(kt, 2, a0, b0); mm(a1, b1);
+    if constexpr (HA) sched(copy_t{}); else sched(nocopy_t{});
+    rd(kt, 3, a1, b1); mm(a0, b0); sched(nocopy_t{});
+    mm(a1, b1);
+    // slice kt+1 has landed (A slice kt+2 may still be in flight) and every
+    // LDS read of slice kt has returned, so after the barrier its units are free
+    if constexpr (HA) wait_vmcnt_lgkm0<INS>();
+    else __builtin_amdgcn_s_waitcnt(0);
+    barrier_no_fence();
+  };
+  using yes = std::integral_constant<bool, true>;
+  using no = std::integral_constant<bool, false>;
+  for (int kt = 0; kt < nk - 2; ++kt) {
+    slice(kt, yes{}, yes{});
+    rd(kt + 1, 0, a0, b0);
+  }
+  slice(nk - 2, yes{}, no{});
+  rd(nk - 1, 0, a0, b0);
+  rd(nk - 1, 1, a1, b1); mm(a0, b0); sched(nocopy_t{});
+  rd(nk - 1, 2, a0, b0); mm(a1, b1); sched(nocopy_t{});
+  rd(nk - 1, 3, a1, b1); mm(a0, b0); sched(nocopy_t{});
+  mm(a1, b1);
+  __syncthreads();  // every wave is done with the ring before the epilogue reuses LDS
+  epilogue_lds_impl<TM>(epi, acc, std::make_index_sequence<TM>{});
+}
+
 typedef __bf16 bf16x8v_t __attribute__((ext_vector_type(8)));
 
 // Small-N projection (the final layer, N = C <= 128): v[m][c] = sum_k A[m][k] W[c][k]
@@ -654,6 +820,7 @@ struct Cfg {
   float eff;
   bool dma;
   void (*fn)(Batch);
+  int min_k;  // smallest K the kernel's pipeline admits
 };
 
 // eff: relative MFMA efficiency of a full tile (measured ordering); the
@@ -662,15 +829,16 @@ struct Cfg {
 #define DIT_DMA_CFG(BM, BN, WGM, WGN, BK_, ST, WPC, EFF)                                      \
   {BM, BN, BN / WGN, WPC, 64 * WGM * WGN, BK_,                                                 \
    kLdsEpilogue<BN / WGN, WGM * WGN, ST * (BM + BN) * BK_ * 2>, EFF, true,                     \
-   gemm_bf16_dma_kernel<BM, BN, WGM, WGN, BK_, ST>}
+   gemm_bf16_dma_kernel<BM, BN, WGM, WGN, BK_, ST>, 0}
 const Cfg kCfgs[] = {
+    {256, 256, 128, 1, 512, 64, true, 1.02f, true, gemm_bf16_ring_kernel, 128},
     DIT_DMA_CFG(256, 256, 4, 2, 64, 2, 1, 1.00f),
     DIT_DMA_CFG(256, 128, 4, 1, 64, 2, 1, 0.72f),
     DIT_DMA_CFG(128, 128, 4, 1, 64, 2, 2, 0.85f),
     DIT_DMA_CFG(32, 256, 1, 4, 64, 2, 2, 0.45f),
-    {256, 128, 128, 1, 256, 64, false, 0.60f, false, gemm_bf16_kernel<256, 128, 4, 1>},
-    {128, 128, 128, 2, 256, 64, false, 0.55f, false, gemm_bf16_kernel<128, 128, 4, 1>},
-    {32, 256, 64, 2, 256, 64, false, 0.30f, false, gemm_bf16_kernel<32, 256, 1, 4>},
+    {256, 128, 128, 1, 256, 64, false, 0.60f, false, gemm_bf16_kernel<256, 128, 4, 1>, 0},
+    {128, 128, 128, 2, 256, 64, false, 0.55f, false, gemm_bf16_kernel<128, 128, 4, 1>, 0},
+    {32, 256, 64, 2, 256, 64, false, 0.30f, false, gemm_bf16_kernel<32, 256, 1, 4>, 0},
 };
 #undef DIT_DMA_CFG
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
@@ -723,7 +891,7 @@ int pick_cfg(const GemmArgs* g, int n, int n_cu) {
     if (!k.dma) return true;
     if (!aligned || !off32 || (k.lds_epi && !epi_ok)) return false;
     for (int i = 0; i < n; ++i)
-      if (g[i].K % k.bk) return false;
+      if (g[i].K % k.bk || g[i].K < k.min_k) return false;
     return true;
   };
   const int f = forced_cfg();

@@ -93,6 +93,31 @@ def test_gemm_qkv_rms_and_gated_residual():
     assert_bf16_close(host_bf16(cbuf), ref)
 
 
+@pytest.mark.parametrize("gated", [False, True])
+def test_gemm_ring_pipeline_ragged(gated):
+    """256 x 256 tiles with the five-slice LDS ring (chosen for this shape:
+    one full wave of 16 x 16 tiles), ragged M and N, K = 320 = five 64-deep
+    slices (prologue, steady slices and the peeled tail); plain and gated
+    residual epilogues against float64."""
+    torch = torch_cuda()
+    M, N, K = 3999, 3992, 320
+    a_b, a = make((M, K))
+    w_b, w = make((N, K), 0.05)
+    b_b, b = make((N,), 0.1)
+    y = a @ w.T + b
+    if not gated:
+        out = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+        binding.gemm_bf16(dev(torch, a_b), dev(torch, w_b), dev(torch, b_b), out, M=M, N=N, K=K)
+        assert_bf16_close(host_bf16(out), round_bf16(y))
+    else:
+        c0_b, c0 = make((M, N))
+        g = RNG.standard_normal(N).astype(np.float32)
+        cbuf = dev(torch, c0_b)
+        binding.gemm_bf16(dev(torch, a_b), dev(torch, w_b), dev(torch, b_b), cbuf, M=M, N=N, K=K,
+                          flags=binding.EPI_GATED_RES, gate=dev(torch, g))
+        assert_bf16_close(host_bf16(cbuf), round_bf16(c0 + g.astype(np.float64) * y))
+
+
 def attn_case(torch, Lq, Lk, heads, sample_rows=None):
     H = heads * 128
     q_b, q = make((Lq, H))
