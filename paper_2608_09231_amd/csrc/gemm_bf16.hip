@@ -238,10 +238,16 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(Batch b) {
 // head is the 16 lanes of one row: 4 shuffles), GELU / SiLU, gated
 // residual, and 8-byte stores that coalesce to 128 bytes per row.
 // Requires N % 8 == 0, gelu_from and gap_at multiples of 4.
+// KIND selects a specialised body: EPI_K_STORE (bf16 store; the per-head RMS
+// norm, GELU and column gap each apply to whole 128-column groups, so they
+// are wave-uniform), EPI_K_GATED (gated residual only), EPI_K_ANY (every
+// flag, per column).
+enum { EPI_K_STORE = 0, EPI_K_GATED = 1, EPI_K_ANY = 2 };
+template <int KIND = EPI_K_ANY>
 struct EpiLds {
   const Prob& P;
   int m_base, ncol0, cq, rq, lrow, lhalf;
-  bool f32out, gated, silu, rms;
+  bool f32out, gated, silu, rms, gelu_u;
   float bv[2][4], gv[2][4];
   int col[2];
   bool ok[2], gl[2];
@@ -255,10 +261,11 @@ struct EpiLds {
     const int lane = lhalf * 32 + lrow;
     cq = lane & 15;
     rq = lane >> 4;
-    f32out = P.flags & DIT_EPI_F32;
-    gated = P.flags & DIT_EPI_GATED_RES;
-    silu = P.flags & DIT_EPI_SILU;
-    rms = ncol0 < P.rms_cols;
+    f32out = KIND == EPI_K_ANY && (P.flags & DIT_EPI_F32);
+    gated = KIND == EPI_K_GATED || (KIND == EPI_K_ANY && (P.flags & DIT_EPI_GATED_RES));
+    silu = KIND == EPI_K_ANY && (P.flags & DIT_EPI_SILU);
+    rms = KIND != EPI_K_GATED && ncol0 < P.rms_cols;
+    gelu_u = KIND == EPI_K_STORE && ncol0 >= P.gelu_from;
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       const int n = ncol0 + 64 * hh + 4 * cq;
@@ -310,7 +317,7 @@ struct EpiLds {
         v[hh][0] = t.x + bv[hh][0]; v[hh][1] = t.y + bv[hh][1];
         v[hh][2] = t.z + bv[hh][2]; v[hh][3] = t.w + bv[hh][3];
       }
-      if (rms) {
+      if (KIND != EPI_K_GATED && rms) {
         float ss = 0.f;
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh)
@@ -325,6 +332,34 @@ struct EpiLds {
           for (int e = 0; e < 4; ++e) v[hh][e] *= sc;
       }
       const int m = m_base + i * 32 + row;
+      if constexpr (KIND == EPI_K_STORE) {
+        if (gelu_u)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[hh][e] = gelu_tanh_f(v[hh][e]);
+        if (m < P.M)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh)
+            if (ok[hh])
+              *(uint2*)((bf16_t*)P.C + (int64_t)m * P.ldc + col[hh]) =
+                  make_uint2(pack_bf16x2(v[hh][0], v[hh][1]), pack_bf16x2(v[hh][2], v[hh][3]));
+        continue;
+      } else if constexpr (KIND == EPI_K_GATED) {
+        if (m < P.M)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh)
+            if (ok[hh]) {
+              const uint2 o = old[p][hh];
+              const float y0 = __uint_as_float(o.x << 16) + gv[hh][0] * v[hh][0];
+              const float y1 = __uint_as_float(o.x & 0xffff0000u) + gv[hh][1] * v[hh][1];
+              const float y2 = __uint_as_float(o.y << 16) + gv[hh][2] * v[hh][2];
+              const float y3 = __uint_as_float(o.y & 0xffff0000u) + gv[hh][3] * v[hh][3];
+              *(uint2*)((bf16_t*)P.C + (int64_t)m * P.ldc + col[hh]) =
+                  make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+            }
+        continue;
+      }
       if (m < P.M) {
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
@@ -359,8 +394,8 @@ struct EpiLds {
 // time when TM > 2) are requested first.
 // Each slab index is a compile-time constant so the accumulators stay in
 // registers.
-template <int TM, size_t... Is>
-__device__ __forceinline__ void epilogue_lds_impl(EpiLds& e, f32x16_t (&acc)[TM][4], std::index_sequence<Is...>) {
+template <int TM, int KIND, size_t... Is>
+__device__ __forceinline__ void epilogue_lds_impl(EpiLds<KIND>& e, f32x16_t (&acc)[TM][4], std::index_sequence<Is...>) {
   if constexpr (TM <= 2) {
     uint2 old[TM][8][2];
     if (e.gated) (e.load_old((int)Is, old[Is]), ...);
@@ -485,7 +520,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
   // The epilogue state (bias, gate, column map) is loaded before the K loop
   // when registers allow (TM <= 2), so those loads are done when the tile is.
-  [[maybe_unused]] EpiLds epi(P, m0 + wm * TM * 32, n0 + wn * 128, lrow, lhalf, (float*)smem + wave * (32 * 128));
+  [[maybe_unused]] EpiLds<> epi(P, m0 + wm * TM * 32, n0 + wn * 128, lrow, lhalf, (float*)smem + wave * (32 * 128));
   if constexpr (kLdsEpilogue<WN, NW, STAGES * STAGE> && TM <= 2) epi.prep();
 
   const int nk = P.K / BK_;
@@ -622,6 +657,7 @@ __device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::
 // the one of the two-stage kernel above (fragments double-buffered in
 // registers, LDS reads of the next substep between the MFMAs).
 // Requires K % 64 == 0, K >= 128 and the LDS-staged epilogue's conditions.
+template <int KIND>
 __global__ __launch_bounds__(512) void gemm_bf16_ring_kernel(Batch b) {
   constexpr int BM = 256, BN = 256, BK_ = 64, WGN = 2;
   constexpr int WM = 64, WN = 128, TM = 2, TN = 4;
@@ -697,7 +733,7 @@ __global__ __launch_bounds__(512) void gemm_bf16_ring_kernel(Batch b) {
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-  EpiLds epi(P, m0 + wm * WM, n0 + wn * WN, lrow, lhalf, (float*)smem + wave * (32 * 128));
+  EpiLds<KIND> epi(P, m0 + wm * WM, n0 + wn * WN, lrow, lhalf, (float*)smem + wave * (32 * 128));
   epi.prep();
   auto mm = [&](const bf16x8_t(&af)[TM], const bf16x8_t(&bfr)[TN]) {
 #pragma unroll
@@ -831,7 +867,7 @@ struct Cfg {
    kLdsEpilogue<BN / WGN, WGM * WGN, ST * (BM + BN) * BK_ * 2>, EFF, true,                     \
    gemm_bf16_dma_kernel<BM, BN, WGM, WGN, BK_, ST>, 0}
 const Cfg kCfgs[] = {
-    {256, 256, 128, 1, 512, 64, true, 1.02f, true, gemm_bf16_ring_kernel, 128},
+    {256, 256, 128, 1, 512, 64, true, 1.02f, true, gemm_bf16_ring_kernel<EPI_K_ANY>, 128},
     DIT_DMA_CFG(256, 256, 4, 2, 64, 2, 1, 1.00f),
     DIT_DMA_CFG(256, 128, 4, 1, 64, 2, 1, 0.72f),
     DIT_DMA_CFG(128, 128, 4, 1, 64, 2, 2, 0.85f),
@@ -946,13 +982,26 @@ hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t stream, int n_
   const int c = pick_cfg(g, n, n_cu);
   if (c < 0) return hipErrorInvalidValue;
   const Cfg& k = kCfgs[c];
+  void (*fn)(Batch) = k.fn;
+  if (fn == gemm_bf16_ring_kernel<EPI_K_ANY>) {
+    bool store = true, gated = true;
+    for (int i = 0; i < n; ++i) {
+      const GemmArgs& a = g[i];
+      const bool plain = !(a.flags & (DIT_EPI_F32 | DIT_EPI_SILU));
+      store &= plain && !(a.flags & DIT_EPI_GATED_RES) && (a.gelu_from >= a.N || a.gelu_from % 128 == 0) &&
+               (a.gap == 0 || a.gap_at % 128 == 0);
+      gated &= plain && (a.flags & DIT_EPI_GATED_RES) && a.rms_cols == 0 && a.gelu_from >= a.N && a.gap == 0;
+    }
+    if (store) fn = gemm_bf16_ring_kernel<EPI_K_STORE>;
+    else if (gated) fn = gemm_bf16_ring_kernel<EPI_K_GATED>;
+  }
   Batch b;
   b.p0 = make_prob(g[0], k.bm, k.bn);
   b.p1 = n > 1 ? make_prob(g[1], k.bm, k.bn) : b.p0;
   b.tiles0 = b.p0.tiles_m * b.p0.tiles_n;
   b.total = b.tiles0 + (n > 1 ? b.p1.tiles_m * b.p1.tiles_n : 0);
   if (b.total == 0) return hipSuccess;
-  hipLaunchKernelGGL(k.fn, dim3(b.total), dim3(k.threads), 0, stream, b);
+  hipLaunchKernelGGL(fn, dim3(b.total), dim3(k.threads), 0, stream, b);
   return hipGetLastError();
 }
 

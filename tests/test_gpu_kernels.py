@@ -118,6 +118,27 @@ def test_gemm_ring_pipeline_ragged(gated):
         assert_bf16_close(host_bf16(cbuf), round_bf16(c0 + g.astype(np.float64) * y))
 
 
+def test_gemm_ring_rms_gelu_gap_ragged():
+    """The ring kernel's store epilogue with the single-block projection's
+    column roles at a ragged M: per-head RMS on the first 2 H columns, GELU
+    on the MLP half, written past a hole of H columns."""
+    torch = torch_cuda()
+    M, H, F, K = 3999, 1024, 1024, 320
+    N, ld = 3 * H + F, 4 * H + F
+    a_b, a = make((M, K))
+    w_b, w = make((N, K), 0.05)
+    b_b, b = make((N,), 0.1)
+    y = a @ w.T + b
+    out = torch.zeros((M, ld), dtype=torch.int16, device="cuda")
+    binding.gemm_bf16(dev(torch, a_b), dev(torch, w_b), dev(torch, b_b), out, M=M, N=N, K=K, ldc=ld,
+                      rms_cols=2 * H, gelu_from=3 * H, gap_at=3 * H, gap=H)
+    got = host_bf16(out)
+    assert_bf16_close(got[:, :2 * H], round_bf16(dit.rms_heads(y[:, :2 * H], 2 * H // 128, 128)))
+    assert_bf16_close(got[:, 2 * H:3 * H], round_bf16(y[:, 2 * H:3 * H]))
+    assert_bf16_close(got[:, 4 * H:], round_bf16(dit.gelu_tanh(y[:, 3 * H:])))
+    assert np.all(got[:, 3 * H:4 * H] == 0)
+
+
 def attn_case(torch, Lq, Lk, heads, sample_rows=None):
     H = heads * 128
     q_b, q = make((Lq, H))
