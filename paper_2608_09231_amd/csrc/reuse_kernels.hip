@@ -29,6 +29,9 @@ namespace {
 constexpr int RR = 16;  // token rows per workgroup (the MFMA's 16 token lanes)
 constexpr int RW = 8;   // waves per workgroup
 constexpr int LPAD = 8; // bf16 elements of padding per LDS row (16 bytes)
+#ifndef EMBED_EB
+#define EMBED_EB 8
+#endif
 
 __device__ __forceinline__ void unpack8(const uint4& u, float (&v)[8]) {
   const uint32_t w[4] = {u.x, u.y, u.z, u.w};
@@ -61,6 +64,15 @@ __device__ __forceinline__ void load_f8(const float* p, float (&m)[8]) {
   m[0] = a.x; m[1] = a.y; m[2] = a.z; m[3] = a.w; m[4] = b.x; m[5] = b.y; m[6] = b.z; m[7] = b.w;
 }
 
+// Workgroup barrier after this wave's LDS operations have completed, without
+// the workgroup-scope fence of __syncthreads (which would also wait for every
+// outstanding global load of the wave).  The memory clobber keeps the
+// compiler from moving memory operations across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+  asm volatile("s_barrier" ::: "memory");
+}
+
 // Copies n16 16-byte vectors global -> LDS with the whole workgroup; every
 // thread issues its loads (up to 8 in flight) before its stores.
 __device__ __forceinline__ void stage(const void* src, void* dst, int n16) {
@@ -82,7 +94,7 @@ __device__ __forceinline__ void stage(const void* src, void* dst, int n16) {
 // operand's 16 token lanes cover the RR rows (lanes past them repeat the
 // last valid row and are not stored).  Lane (lr, lq) ends with
 // h[row lr][16 j + 4 lq + i], i = 0..3: one 8-byte LDS store.
-template <int CK>
+template <int CK, int EB>
 __device__ __forceinline__ void embed_to_lds(const float* __restrict__ x, int C, const bf16_t* __restrict__ W,
                                              const bf16_t* bl, int row0, int rows, int H, bf16_t* hl, int ldl,
                                              int wave, int lane) {
@@ -98,14 +110,19 @@ __device__ __forceinline__ void embed_to_lds(const float* __restrict__ x, int C,
   const bool store = lr < RR && row0 + lr < rows;
   // W_in tiles stream from L2 in batches of EB, the next batch in flight
   // while the current one is multiplied and stored
-  constexpr int EB = 4;
-  const int ntile = H / 16;  // tiles j = wave + RW * u
-  const int nu = (ntile - wave + RW - 1) / RW;
+  // Each wave takes a contiguous run of tiles when they divide evenly (its
+  // W_in rows then spread over every L2 channel), else tiles wave + RW u.
+  const int ntile = H / 16;
+  const bool contig = ntile % RW == 0;
+  const int nu = contig ? ntile / RW : (ntile - wave + RW - 1) / RW;
   uint4 wcur[EB][CK], wnxt[EB][CK];
   // every workgroup walks its tiles from a different start, so the CUs of an
   // XCD do not all request the same L2 lines at the same time
   const int rot = blockIdx.x % nu;
-  auto tile_of = [&](int u) { const int v = u + rot; return wave + RW * (v < nu ? v : v - nu); };
+  auto tile_of = [&](int u) {
+    const int v = u + rot, w = v < nu ? v : v - nu;
+    return contig ? wave * nu + w : wave + RW * w;
+  };
   auto load_batch = [&](int u0, uint4 (&w)[EB][CK]) {
 #pragma unroll
     for (int e = 0; e < EB; ++e) {
@@ -188,10 +205,15 @@ __global__ __launch_bounds__(64 * RW) void reuse_indicator_kernel(
     stage(sh, shl, H / 4);
   }
   const bool same = m_prev == m_last;
+  lds_barrier();
+  embed_to_lds<CK, EMBED_EB>(x, C, W_in, bl, row0, rows, H, hl, ldl, wave, lane);
 
-  // the previous indicator rows stream in while the embedding runs
-  // (addresses clamped into the tensors so every load is unconditional and
-  // they all issue back to back; out-of-range chunks and rows are not used)
+  // The previous indicator rows are requested only now: vector loads retire
+  // in issue order, so had they been issued before the embedding, its first
+  // wait for W_in would have waited for them too.  They stream in while m_t
+  // is computed and stored (addresses clamped into the tensors so every load
+  // is unconditional and they all issue back to back; out-of-range chunks
+  // and rows are not used).
   uint4 pv[RPW][MAXC], lv[RPW][MAXC];
   if (sums) {
 #pragma unroll
@@ -205,18 +227,16 @@ __global__ __launch_bounds__(64 * RW) void reuse_indicator_kernel(
       }
     }
   }
+  lds_barrier();  // the h tile is complete; the row loads stay in flight
 
-  __syncthreads();
-  embed_to_lds<CK>(x, C, W_in, bl, row0, rows, H, hl, ldl, wave, lane);
-  __syncthreads();
-
-  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  // pass 1: m_t rows (or h rows on a full step), values kept for the sums
+  uint4 mt[RPW][MAXC];
 #pragma unroll
   for (int q = 0; q < RPW; ++q) {
     const int rr = wave + RW * q, row = row0 + rr;
-    if (row >= rows) break;
     const bf16_t* src = hl + rr * ldl;
     if (h_out) {  // block-stack input of a full step
+      if (row >= rows) continue;
 #pragma unroll
       for (int j = 0; j < MAXC; ++j) {
         const int c = lane + 64 * j;
@@ -238,41 +258,50 @@ __global__ __launch_bounds__(64 * RW) void reuse_indicator_kernel(
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
       const int c = lane + 64 * j;
-      if (c >= nch) continue;
       float y[8];
       if (sc) {
         float a[8], bsh[8];
-        load_f8(scl + 8 * c, a);
-        load_f8(shl + 8 * c, bsh);
+        load_f8(scl + 8 * min(c, nch - 1), a);
+        load_f8(shl + 8 * min(c, nch - 1), bsh);
 #pragma unroll
         for (int e = 0; e < 8; ++e) y[e] = (v[j][e] - mean) * rstd * (1.f + a[e]) + bsh[e];
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) y[e] = v[j][e];
       }
-      const uint4 packed = pack8(y);
-      st_stream(m_out + (int64_t)row * H + 8 * c, packed);
-      if (sums) {
-        float mv[8], p[8], l[8];
-        unpack8(packed, mv);  // the stored (rounded) m_t
-        unpack8(pv[q][j], p);
-        if (same) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) l[e] = p[e];
-        } else {
-          unpack8(lv[q][j], l);
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          a0 += fabsf(mv[e] - p[e]);
-          a1 += fabsf(p[e]);
-          a2 += fabsf(mv[e] - l[e]);
-          a3 += fabsf(l[e]);
-        }
-      }
+      mt[q][j] = pack8(y);
+      if (c < nch && row < rows) st_stream(m_out + (int64_t)row * H + 8 * c, mt[q][j]);
     }
   }
   if (!sums) return;
+  // pass 2: relative-L1 sums against the stored (rounded) m_t
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+  for (int q = 0; q < RPW; ++q) {
+    const int row = row0 + wave + RW * q;
+    if (row >= rows) break;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+      const int c = lane + 64 * j;
+      if (c >= nch) continue;
+      float mv[8], p[8], l[8];
+      unpack8(mt[q][j], mv);
+      unpack8(pv[q][j], p);
+      if (same) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) l[e] = p[e];
+      } else {
+        unpack8(lv[q][j], l);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        a0 += fabsf(mv[e] - p[e]);
+        a1 += fabsf(p[e]);
+        a2 += fabsf(mv[e] - l[e]);
+        a3 += fabsf(l[e]);
+      }
+    }
+  }
   a0 = warp_sum(a0); a1 = warp_sum(a1); a2 = warp_sum(a2); a3 = warp_sum(a3);
   if (lane == 0) { red[wave][0] = a0; red[wave][1] = a1; red[wave][2] = a2; red[wave][3] = a3; }
   __syncthreads();
@@ -314,13 +343,13 @@ __global__ __launch_bounds__(64 * RW) void reuse_final_kernel(
 #pragma unroll
       for (int j = 0; j < MAXC; ++j) rv[q][j] = ld_stream(rb + (int64_t)row * H + 8 * min(lane + 64 * j, nch - 1));
     }
-    if (b) __syncthreads();  // the previous branch's projection is done with the tile
+    if (b) lds_barrier();  // the previous branch's projection is done with the tile
     if (b == 0) stage(b_in, bl, H / 8);
     stage(mod + H, scl, H / 4);
     stage(mod, shl, H / 4);
-    __syncthreads();
-    embed_to_lds<CK>(x, C, W_in, bl, row0, rows, H, hl, ldl, wave, lane);
-    __syncthreads();
+    lds_barrier();
+    embed_to_lds<CK, 4>(x, C, W_in, bl, row0, rows, H, hl, ldl, wave, lane);
+    lds_barrier();
     // h_out = S(h + r), y = S(LN(h_out)(1 + sc) + sh), in place
 #pragma unroll
     for (int q = 0; q < RPW; ++q) {
@@ -351,7 +380,7 @@ __global__ __launch_bounds__(64 * RW) void reuse_final_kernel(
         *(uint4*)(src + 8 * c) = pack8(y);
       }
     }
-    __syncthreads();
+    lds_barrier();
     // v^T = W_out y^T: lane (lr, lq) of tile j ends with v[row lr][16 j + 4 lq + i].
     // KS waves share a tile, each a contiguous K range; partial sums meet in
     // LDS and are added in wave order.
@@ -387,7 +416,7 @@ __global__ __launch_bounds__(64 * RW) void reuse_final_kernel(
 #pragma unroll
       for (int i = 0; i < 4; ++i) vpart[wave][lane][i] = (acc[0][i] + acc[1][i]) + (acc[2][i] + acc[3][i]);
     }
-    __syncthreads();
+    lds_barrier();
     if (wave < NT) {
       const uint2 bb = *(const uint2*)(b_out + 16 * wave + 4 * lq);
       const float bias[4] = {__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xffff0000u),
