@@ -13,8 +13,14 @@
 // With bounded logits (unit-gain RMS-normalised q and k) a fixed shift
 // replaces the running max; the row sum takes the bf16-rounded P with a
 // packed dot product.  Exact-softmax semantics (non-causal), f32 statistics,
-// output normalised once at the end.
+// output normalised once at the end.  The sampler's bounded-logit launches
+// use a software-pipelined form of the same arithmetic (flash_attn_pipe_kernel):
+// each iteration overlaps the softmax of one key tile (VALU) with the PV
+// product of the previous tile and the score product of the next (MFMA).
 #include <math.h>
+#include <stdlib.h>
+
+#include <string>
 
 #include "common.h"
 #include "kernels.h"
@@ -258,6 +264,187 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
   }
 }
 
+// Software-pipelined variant (bounded logits only): iteration t runs the
+// PV product of tile t-1 and the score product of tile t+1 (MFMA) together
+// with the softmax of tile t (VALU), which depends on neither.  Five LDS
+// stages: tiles t-1 (V), t, t+1 (K), t+2 and t+3 (in flight).
+constexpr int PSTAGE = 5;
+template <int NW>
+__global__ __launch_bounds__(64 * NW) void flash_attn_pipe_kernel(
+    const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restrict__ k, int64_t ldk,
+    const bf16_t* __restrict__ vt, int ldvt, bf16_t* __restrict__ o, int64_t ldo, int Lq, int Lk,
+    float scale_log2, SeqMap sm) {
+  __shared__ __attribute__((aligned(1024))) char smem[PSTAGE][TILE_BYTES];  // [stage][K | V^T]
+  const RowMap rm = sm.at(blockIdx.z);
+  vt += (int64_t)blockIdx.z * gridDim.y * D * ldvt;
+
+  constexpr int QB = NW * 32;
+  constexpr int CPW = 16 / NW;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lrow = lane & 31, lhalf = lane >> 5;
+  const int h = blockIdx.y;
+  const int q0 = blockIdx.x * QB + wave * 32;
+
+  bf16x8_t qf[8];
+  {
+    const int qr = min(q0 + lrow, Lq - 1);
+    const bf16_t* qp = q + rm(qr) * ldq + h * D + 8 * lhalf;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qf[s] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(qp + 16 * s));
+  }
+  const bf16_t* kh = k + h * D;
+  const bf16_t* vh = vt + (int64_t)h * D * ldvt;
+  auto issue_tile = [&](int t) {
+    const int kb0 = t * KT;
+    char* sk = smem[t % PSTAGE];
+    char* sv = sk + KT * D * 2;
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) {
+      const int ii = wave * CPW + j;
+      {
+        const int row = 4 * ii + (lane >> 4);
+        const int c = (lane & 15) ^ (row & 15);
+        const int key = min(kb0 + row, Lk - 1);
+        __builtin_amdgcn_global_load_lds((glb_void_t*)(kh + rm(key) * ldk + c * 8),
+                                         (lds_void_t*)(sk + ii * 1024), 16, 0, 0);
+      }
+      {
+        const int d = 8 * ii + (lane >> 3);
+        const int c = (lane & 7) ^ ((d >> 1) & 7);
+        __builtin_amdgcn_global_load_lds((glb_void_t*)(vh + (int64_t)d * ldvt + kb0 + c * 8),
+                                         (lds_void_t*)(sv + ii * 1024), 16, 0, 0);
+      }
+    }
+  };
+  auto scores = [&](int t, f32x16_t (&sacc)[2]) {
+    const char* sk = smem[t % PSTAGE];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sk + k_off(kb * 32 + lrow, 2 * s + lhalf)));
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
+      }
+  };
+  f32x16_t oacc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
+  float l_run = 0.f;
+  const float mneg = -BOUNDED_SHIFT_LOG2;
+  const bf16x2_t ones = {(__bf16)1.f, (__bf16)1.f};
+  auto softmax = [&](int t, f32x16_t (&sacc)[2], bf16x8_t (&pf)[4], bool ragged) {
+    const int kbase = t * KT;
+    if (ragged) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kbase + kb * 32 + 8 * (r >> 2) + 4 * lhalf + (r & 3);
+          if (key >= Lk) sacc[kb][r] = -INFINITY;
+        }
+    }
+    float ls = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      uint32_t w[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][2 * j], scale_log2, mneg));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][2 * j + 1], scale_log2, mneg));
+        w[j] = pack_bf16x2(p0, p1);
+        ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w[j]), ones, ls, false);
+      }
+      pf[2 * kb] = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
+      pf[2 * kb + 1] = __builtin_bit_cast(bf16x8_t, make_uint4(w[4], w[5], w[6], w[7]));
+    }
+    l_run += ls;
+  };
+  auto pv = [&](int t, const bf16x8_t (&pf)[4]) {
+    const char* sv = smem[t % PSTAGE] + KT * D * 2;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sv + v_off(dt * 32 + lrow, 2 * ks + lhalf)));
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], oacc[dt], 0, 0, 0);
+      }
+  };
+  // wait until tile u has landed: tiles issued after it may stay in flight
+  auto wait_tile = [&](int u, int issued) {  // issued = tiles issued so far (0..issued-1)
+    const int later = issued - 1 - u;
+    if (later >= 2) __builtin_amdgcn_s_waitcnt((2 * 2 * CPW) | (7 << 4) | (0 << 8));
+    else if (later == 1) __builtin_amdgcn_s_waitcnt((2 * CPW) | (7 << 4) | (0 << 8));
+    else __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("s_barrier" ::: "memory");
+  };
+
+  const int ntiles = (Lk + KT - 1) / KT;
+  f32x16_t s_cur[2], s_nxt[2];
+  bf16x8_t p_prv[4], p_cur[4];
+  // generic iteration (prologue and tail): every part guarded
+  auto iter_any = [&](int t) {
+    if (t + 3 < ntiles) issue_tile(t + 3);
+    if (t > 0) pv(t - 1, p_prv);
+    if (t + 1 < ntiles) scores(t + 1, s_nxt);
+    softmax(t, s_cur, p_cur, t * KT + KT > Lk);
+    // tile t+2 must have landed for the next iteration's scores; tile t+3 may stay in flight
+    if (t + 3 < ntiles) __builtin_amdgcn_s_waitcnt((2 * CPW) | (7 << 4) | (0 << 8));
+    else __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("s_barrier" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p_prv[i] = p_cur[i];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) s_cur[kb] = s_nxt[kb];
+  };
+  // steady iteration: 0 < t, t + 3 < ntiles, tile t full
+  auto iter_steady = [&](int t) {
+    issue_tile(t + 3);
+    pv(t - 1, p_prv);
+    scores(t + 1, s_nxt);
+    softmax(t, s_cur, p_cur, false);
+    __builtin_amdgcn_s_waitcnt((2 * CPW) | (7 << 4) | (0 << 8));
+    asm volatile("s_barrier" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p_prv[i] = p_cur[i];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) s_cur[kb] = s_nxt[kb];
+  };
+  for (int u = 0; u < 3 && u < ntiles; ++u) issue_tile(u);
+  // tiles 0 and 1 have landed (tile 2 may stay in flight)
+  if (ntiles >= 3) __builtin_amdgcn_s_waitcnt((2 * CPW) | (7 << 4) | (0 << 8));
+  else __builtin_amdgcn_s_waitcnt(0);
+  asm volatile("s_barrier" ::: "memory");
+  scores(0, s_cur);
+  iter_any(0);
+  int t = 1;
+  for (; t + 3 < ntiles; ++t) iter_steady(t);
+  for (; t < ntiles; ++t) iter_any(t);
+  pv(ntiles - 1, p_prv);
+
+  {
+    const int qi = q0 + lrow;
+    const float l = l_run + __shfl_xor(l_run, 32, 64);
+    const float inv = 1.f / l;
+    if (qi < Lq) {
+      bf16_t* op = o + rm(qi) * ldo + h * D;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int d0 = dt * 32 + 8 * r4 + 4 * lhalf;
+          *(uint2*)(op + d0) = make_uint2(pack_bf16x2(oacc[dt][4 * r4] * inv, oacc[dt][4 * r4 + 1] * inv),
+                                          pack_bf16x2(oacc[dt][4 * r4 + 2] * inv, oacc[dt][4 * r4 + 3] * inv));
+        }
+    }
+  }
+}
+
 // vt[h][d][16 g + vt_slot(k)] = v[16 g + k][h*128 + d] for keys < Lk, 0 up to ldvt.
 __global__ __launch_bounds__(256) void transpose_v_kernel(const bf16_t* __restrict__ v, int64_t ldv,
                                                           bf16_t* __restrict__ vt, int Lk, int ldvt, SeqMap sm) {
@@ -353,7 +540,16 @@ hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
   const dim3 grid((Lq + QB - 1) / QB, heads, nseq);
   const SeqMap sm{split, gap, gz, zs};
-  if (bounded_logits)
+  // bounded logits take the software-pipelined kernel; DIT_ATTN_KERNEL=base
+  // selects the single-stage one (experiments)
+  static const bool pipe = [] {
+    const char* e = getenv("DIT_ATTN_KERNEL");
+    return !(e && std::string(e) == "base");
+  }();
+  if (bounded_logits && pipe)
+    hipLaunchKernelGGL((flash_attn_pipe_kernel<kNW>), grid, dim3(64 * kNW), 0, s, (const bf16_t*)q, ldq,
+                       (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o, ldo, Lq, Lk, scale_log2, sm);
+  else if (bounded_logits)
     hipLaunchKernelGGL((flash_attn_bf16_kernel<true, kQG, kNW>), grid, dim3(64 * kNW), 0, s,
                        (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o,
                        ldo, Lq, Lk, scale_log2, sm);
