@@ -265,13 +265,14 @@ dit_status ln_mod(dit_cache* c, const void* x, int64_t ldx, void* out, int64_t l
 
 // attention over joint rows: q,k,v inside Y (or separate), output into o;
 // nseq stacked sequences in one launch (bf16; see launch_flash_attn_bf16)
+// vt_ready: the projection has already written the transposed values into vt_ws
 dit_status attention(dit_cache* c, const void* q, int64_t ldq, const void* k, int64_t ldk, const void* v,
                      int64_t ldv, void* o, int64_t ldo, int Lq, int Lk, void* vt_ws, int split = 0x7fffffff,
-                     int64_t gap = 0, int nseq = 1, int64_t zs = 0, int64_t gz = 0) {
+                     int64_t gap = 0, int nseq = 1, int64_t zs = 0, int64_t gz = 0, bool vt_ready = false) {
   const int heads = c->cfg.heads, hd = c->cfg.head_dim;
   const double flops = 4.0 * Lq * (double)Lk * heads * hd * nseq;
   if (c->bf16) {
-    {
+    if (!vt_ready) {
       Scope s(c, DIT_K_FULL_OTHER, 2.0 * Lk * heads * hd * 2 * nseq);
       HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt_ws, Lk, heads, c->stream, split, gap, nseq, zs, gz));
     }
@@ -404,7 +405,13 @@ dit_status ensure_seq(dit_cache* c, int Q) {
   TRY(dalloc(c, &c->X, LB * c->H * e));
   TRY(dalloc(c, &c->A, LB * c->H * e));
   TRY(dalloc(c, &c->Y, LB * c->ldY * e));
-  if (c->bf16) TRY(dalloc(c, &c->vt, (size_t)Q * c->cfg.heads * 128 * rup(c->L, 64) * 2));
+  if (c->bf16) {
+    // keys past L stay zero for good: attention reads whole 64-key tiles, and
+    // the projection that writes the transposed values never touches them
+    const size_t vb = (size_t)Q * c->cfg.heads * 128 * rup(c->L, 64) * 2;
+    TRY(dalloc(c, &c->vt, vb));
+    HIPCK(hipMemsetAsync(c->vt, 0, vb, c->stream));
+  }
   if (c->stacked && c->cfg.pooled_text) TRY(dalloc(c, &c->modq, (size_t)Q * c->n_mod * 4));
   c->cap_seq = Q;
   return DIT_OK;
@@ -795,9 +802,23 @@ dit_status full_stack_multi(dit_cache* c, const Seq* seqs, int Q) {
     return ln_mod(c, c->X, H, c->A, H, LL, Lt, b + ot, b + ot + H, b + oi, b + oi + H, DIT_K_FULL_OTHER, Nt, N,
                   mr.d);
   };
-  auto attn = [&]() {
+  auto attn = [&](bool vt_ready) {
     return attention(c, c->Y, ldY, sp(c, c->Y, H), ldY, sp(c, c->Y, 2 * H), ldY, sp(c, c->Y, 3 * H), ldY, L, L,
-                     c->vt, Nt, (int64_t)(Q - 1) * Nt, Q, Nt, (int64_t)N - Nt);
+                     c->vt, Nt, (int64_t)(Q - 1) * Nt, Q, Nt, (int64_t)N - Nt, vt_ready);
+  };
+  // The QKV projection writes the values transposed for attention itself
+  // (layout [sequence][head][128][rup(L, 64)], the keys of a sequence being
+  // its text rows then its image rows) when the GEMM admits it; otherwise
+  // they are stored in Y and transposed by a separate pass.
+  const int ldvt = (int)rup(L, 64);
+  auto with_vt = [&](GemmArgs& g, int rows0, int key0, int split = 0x7fffffff, int rows1 = 1, int key1 = 0) {
+    g.vt = c->vt;
+    g.vt_col0 = 2 * H;
+    g.vt_heads = c->cfg.heads;
+    g.vt_ld = ldvt;
+    g.vt_split = split;
+    g.vt_rows0 = rows0; g.vt_key0 = key0;
+    g.vt_rows1 = rows1; g.vt_key1 = key1;
   };
   for (int i = 0; i < c->cfg.n_double; ++i) {
     const DoubleW& w = c->M.dbl[i];
@@ -807,8 +828,12 @@ dit_status full_stack_multi(dit_cache* c, const Seq* seqs, int Q) {
     g[0] = lin_args(c, Ai, H, w.qkv[0], Yi, ldY, Li);
     g[1] = lin_args(c, c->A, H, w.qkv[1], c->Y, ldY, Lt);
     g[0].rms_cols = g[1].rms_cols = 2 * H;
+    with_vt(g[0], N, Nt);   // image rows: keys Nt .. Nt + N - 1 of sequence m / N
+    with_vt(g[1], Nt, 0);   // text rows: keys 0 .. Nt - 1 of sequence m / Nt
+    const bool vt_fused = dit::gemm_bf16_fuses_vt(g, 2, c->n_cu);
+    if (!vt_fused) g[0].vt = g[1].vt = nullptr;
     TRY(gemm(c, g, 2, cls));
-    TRY(attn());
+    TRY(attn(vt_fused));
     TRY(gated(lin_args(c, Yi + 3 * H * es, ldY, w.o[0], Xi, H, Li, DIT_EPI_GATED_RES),
               lin_args(c, sp(c, c->Y, 3 * H), ldY, w.o[1], c->X, H, Lt, DIT_EPI_GATED_RES), mi + 2 * H,
               mt + 2 * H));
@@ -830,8 +855,11 @@ dit_status full_stack_multi(dit_cache* c, const Seq* seqs, int Q) {
     g.gelu_from = 3 * H;
     g.gap_at = 3 * H;
     g.gap = H;
+    with_vt(g, Nt, 0, Lt, N, Nt);  // the Q text row blocks, then the Q image row blocks
+    const bool vt_fused = dit::gemm_bf16_fuses_vt(&g, 1, c->n_cu);
+    if (!vt_fused) g.vt = nullptr;
     TRY(gemm(c, &g, 1, cls));
-    TRY(attn());
+    TRY(attn(vt_fused));
     if (mr.d == 0) {
       g = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.l2, c->X, H, LL, DIT_EPI_GATED_RES);
       g.gate = mr.base + ms + 2 * H;

@@ -36,6 +36,8 @@ struct Prob {
   int M, N, K;
   int flags, rms_cols, gelu_from, gap_at, gap, gseg;
   int tiles_m, tiles_n;
+  bf16_t* vt;  // transposed values (see GemmArgs)
+  int vt_col0, vt_heads, vt_ld, vt_split, vt_rows0, vt_key0, vt_rows1, vt_key1;
 };
 
 struct Batch {
@@ -634,6 +636,48 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
   }
 }
 
+// Transposed values straight from the accumulators of a wave that owns 64
+// rows x one 128-column head group (TM = 2, TN = 4).  In a 32 x 32 block,
+// lane (lrow, lhalf) holds column lrow and rows 8 (r / 4) + 4 lhalf + r % 4;
+// with the key order of the transposed layout (slot 8 ((k >> 2) & 1) +
+// 4 (k >> 3) + (k & 3) inside each 16-key group) its registers r = 0..7 are
+// slots 8 lhalf .. 8 lhalf + 7 of the first group and r = 8..15 the same
+// slots of the second, so each lane stores two 16-byte runs per block.  The
+// host admits this only for 32-row aligned segments (a block is one
+// sequence's keys kb .. kb + 31, kb a multiple of 32).
+__device__ __forceinline__ void store_vt(const Prob& P, const f32x16_t (&acc)[2][4], int m_base, int ncol0,
+                                         int lrow, int lhalf) {
+  const int h = (ncol0 - P.vt_col0) >> 7;
+  float bias[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) bias[j] = P.bias ? bf16_to_f32(P.bias[ncol0 + 32 * j + lrow]) : 0.f;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int m = m_base + 32 * i;
+    if (m >= P.M) continue;
+    int z, key;
+    if (m < P.vt_split) {
+      z = m / P.vt_rows0;
+      key = P.vt_key0 + m % P.vt_rows0;
+    } else {
+      const int mm = m - P.vt_split;
+      z = mm / P.vt_rows1;
+      key = P.vt_key1 + mm % P.vt_rows1;
+    }
+    bf16_t* base = P.vt + ((int64_t)(z * P.vt_heads + h) * 128 + lrow) * P.vt_ld + key + 8 * lhalf;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const f32x16_t& a = acc[i][j];
+      const float b = bias[j];
+      bf16_t* row = base + (int64_t)(32 * j) * P.vt_ld;
+      *(uint4*)row = make_uint4(pack_bf16x2(a[0] + b, a[1] + b), pack_bf16x2(a[2] + b, a[3] + b),
+                                pack_bf16x2(a[4] + b, a[5] + b), pack_bf16x2(a[6] + b, a[7] + b));
+      *(uint4*)(row + 16) = make_uint4(pack_bf16x2(a[8] + b, a[9] + b), pack_bf16x2(a[10] + b, a[11] + b),
+                                       pack_bf16x2(a[12] + b, a[13] + b), pack_bf16x2(a[14] + b, a[15] + b));
+    }
+  }
+}
+
 // vmcnt(N) and lgkmcnt(0) in one wait (same encoding as wait_vmcnt).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt_lgkm0() {
@@ -796,6 +840,13 @@ __global__ __launch_bounds__(512) void gemm_bf16_ring_kernel(Batch b) {
   rd(nk - 1, 3, a1, b1); mm(a0, b0); sched(nocopy_t{});
   mm(a1, b1);
   __syncthreads();  // every wave is done with the ring before the epilogue reuses LDS
+  if constexpr (KIND == EPI_K_STORE) {
+    const int ncol0 = n0 + wn * WN;  // wave-uniform: whole head groups are values or not
+    if (P.vt && ncol0 >= P.vt_col0 && ncol0 < P.vt_col0 + 128 * P.vt_heads) {
+      store_vt(P, acc, m0 + wm * WM, ncol0, lrow, lhalf);
+      return;
+    }
+  }
   epilogue_lds_impl<TM>(epi, acc, std::make_index_sequence<TM>{});
 }
 
@@ -892,6 +943,9 @@ Prob make_prob(const GemmArgs& g, int bm, int bn) {
   p.gelu_from = g.gelu_from; p.gap_at = g.gap_at; p.gap = g.gap;
   p.tiles_m = (g.M + bm - 1) / bm;
   p.tiles_n = (g.N + bn - 1) / bn;
+  p.vt = (bf16_t*)g.vt;
+  p.vt_col0 = g.vt_col0; p.vt_heads = g.vt_heads; p.vt_ld = g.vt_ld; p.vt_split = g.vt_split;
+  p.vt_rows0 = g.vt_rows0; p.vt_key0 = g.vt_key0; p.vt_rows1 = g.vt_rows1; p.vt_key1 = g.vt_key1;
   return p;
 }
 
@@ -974,15 +1028,10 @@ hipError_t launch_proj_small_n(const void* A, int64_t lda, const void* W, int64_
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t stream, int n_cu) {
-  if (n < 1 || n > 2) return hipErrorInvalidValue;
-  for (int i = 0; i < n; ++i)
-    if (g[i].gseg < 0 || (g[i].gseg > 0 && (g[i].gseg % 32 || !(g[i].flags & DIT_EPI_GATED_RES))))
-      return hipErrorInvalidValue;
-  const int c = pick_cfg(g, n, n_cu);
-  if (c < 0) return hipErrorInvalidValue;
-  const Cfg& k = kCfgs[c];
-  void (*fn)(Batch) = k.fn;
+// The kernel for these problems (config c): the 256 x 256 ring kernel takes
+// a specialised epilogue when every problem admits it.
+static void (*kernel_for(const GemmArgs* g, int n, int c))(Batch) {
+  void (*fn)(Batch) = kCfgs[c].fn;
   if (fn == gemm_bf16_ring_kernel<EPI_K_ANY>) {
     bool store = true, gated = true;
     for (int i = 0; i < n; ++i) {
@@ -995,6 +1044,43 @@ hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t stream, int n_
     if (store) fn = gemm_bf16_ring_kernel<EPI_K_STORE>;
     else if (gated) fn = gemm_bf16_ring_kernel<EPI_K_GATED>;
   }
+  return fn;
+}
+
+// The transposed-value output: the store kernel, head groups inside the
+// output, no column gap or GELU or RMS over them, 32-row aligned segments
+// and key offsets, and 16-byte aligned rows of vt.
+static bool vt_ok(const GemmArgs* g, int n, int c) {
+  if (c < 0 || kernel_for(g, n, c) != gemm_bf16_ring_kernel<EPI_K_STORE>) return false;
+  for (int i = 0; i < n; ++i) {
+    const GemmArgs& a = g[i];
+    if (!a.vt) continue;
+    const int end = a.vt_col0 + 128 * a.vt_heads;
+    if (a.vt_heads < 1 || a.vt_col0 % 128 || end > a.N || a.vt_ld % 8 || ((uintptr_t)a.vt & 15)) return false;
+    if (a.vt_col0 < a.rms_cols || end > a.gelu_from || (a.gap && end > a.gap_at)) return false;
+    if (a.M % 32 || a.vt_rows0 % 32 || a.vt_key0 % 32 || a.vt_rows0 < 1) return false;
+    if (a.vt_split < a.M && (a.vt_split % 32 || a.vt_rows1 % 32 || a.vt_key1 % 32 || a.vt_rows1 < 1)) return false;
+  }
+  return true;
+}
+
+bool gemm_bf16_fuses_vt(const GemmArgs* g, int n, int n_cu) {
+  if (n < 1 || n > 2) return false;
+  return vt_ok(g, n, pick_cfg(g, n, n_cu));
+}
+
+hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t stream, int n_cu) {
+  if (n < 1 || n > 2) return hipErrorInvalidValue;
+  for (int i = 0; i < n; ++i)
+    if (g[i].gseg < 0 || (g[i].gseg > 0 && (g[i].gseg % 32 || !(g[i].flags & DIT_EPI_GATED_RES))))
+      return hipErrorInvalidValue;
+  const int c = pick_cfg(g, n, n_cu);
+  if (c < 0) return hipErrorInvalidValue;
+  bool want_vt = false;
+  for (int i = 0; i < n; ++i) want_vt |= g[i].vt != nullptr;
+  if (want_vt && !vt_ok(g, n, c)) return hipErrorInvalidValue;
+  const Cfg& k = kCfgs[c];
+  void (*fn)(Batch) = kernel_for(g, n, c);
   Batch b;
   b.p0 = make_prob(g[0], k.bm, k.bn);
   b.p1 = n > 1 ? make_prob(g[1], k.bm, k.bn) : b.p0;

@@ -24,11 +24,27 @@ struct GemmArgs {
   // gate + (m / gseg) * gstride.  gseg = 0: one vector; else a multiple of 32.
   int gseg = 0;
   int64_t gstride = 0;
+  // Values transposed for attention (vt != nullptr): output columns
+  // [vt_col0, vt_col0 + 128 vt_heads) are not stored in C but written, with
+  // bias and bf16 rounding as usual, as vt[z][head][d][key] with row stride
+  // vt_ld and the key order of launch_transpose_v_bf16 (permuted inside
+  // 16-key groups).  Output row m (m < vt_split: segment 0, else segment 1
+  // with m - vt_split) of a segment with R rows per sequence and key offset
+  // k0 goes to sequence m / R, key k0 + m % R.
+  void* vt = nullptr;
+  int vt_col0 = 0, vt_heads = 0, vt_ld = 0;
+  int vt_split = 0x7fffffff;
+  int vt_rows0 = 1, vt_key0 = 0, vt_rows1 = 1, vt_key1 = 0;
 };
 
 // bf16 MFMA GEMM; n = 1 or 2 independent problems in one launch.  Invalid
 // arguments (no tile configuration admits the problem) return an error.
 hipError_t launch_gemm_bf16(const GemmArgs* g, int n, hipStream_t s, int n_cu);
+// Whether launch_gemm_bf16 can write the transposed values of these problems
+// itself (the vt fields set): 128-column head groups, 32-row aligned segments
+// and the 256 x 256 kernel.  Otherwise the caller leaves vt unset and
+// transposes the values with launch_transpose_v_bf16.
+bool gemm_bf16_fuses_vt(const GemmArgs* g, int n, int n_cu);
 // v = A W^T + bias for N <= 128 (multiple of 16), K % 32 == 0, f32 output; with
 // x != nullptr the result goes into the Euler update x += alpha * v instead.
 hipError_t launch_proj_small_n(const void* A, int64_t lda, const void* W, int64_t ldw, const void* bias,
