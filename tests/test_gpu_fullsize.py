@@ -164,3 +164,37 @@ def test_attention_long_sequences_sampled(L, heads, label):
     err = rel_l2(got[rows], ref)
     say(f"{label} attention L={L}: sampled rel-L2 {err:.2e}")
     assert err < 4e-3
+
+
+def test_flux1024_width_two_prompts_stacked():
+    """Two FLUX-1024 prompts (one double and one single block, full width and
+    tokens) through the stacked multi-prompt path: every launch of the block
+    stack carries both sequences, including the QKV projections that write
+    the transposed values per sequence (text rows, then image rows).  Each
+    prompt must match the library's single-sample run on the same schedule
+    (whose parity with the oracle the one-block test above checks)."""
+    torch = torch_cuda()
+    w = synth.reduced(synth.workload("flux1024"), T=3, B=2, n_double=1, n_single=1)
+    cfg = w.model
+    weights, _, _, gate = synth.make_inputs(w)
+    x0 = np.stack([synth.make_latent(cfg, w.seed + 101 * j) for j in range(2)])
+    text = np.stack([synth.make_text(cfg, w.seed + 211 * j + 1) for j in range(2)])
+    h = binding.DitCache(cfg, weights.blob)
+    try:
+        lat = dev(torch, x0.astype(np.float32))
+        scheds = h.sample_batch(lat, dev(torch, text), gate, w.T, w.B, shift=w.shift,
+                                forced_masks=np.ones((2, w.T), np.uint8) * np.array([1, 1, 0], np.uint8))
+        torch.cuda.synchronize()
+        xb = lat.cpu().numpy().astype(np.float64)
+        for j in range(2):
+            lj = dev(torch, x0[j].astype(np.float32))
+            sj = h.sample(lj, dev(torch, text[j]), gate, w.T, w.B, shift=w.shift, forced_mask=scheds[j].full)
+            torch.cuda.synchronize()
+            xj = lj.cpu().numpy().astype(np.float64)
+            np.testing.assert_array_equal(sj.full, scheds[j].full)
+            err = rel_l2(xb[j], xj)
+            say(f"two prompts: prompt {j} batch vs alone rel-L2 {err:.3e}")
+            assert err <= 5e-3
+            np.testing.assert_allclose(scheds[j].sums[1:], sj.sums[1:], rtol=1e-3)
+    finally:
+        h.close()
