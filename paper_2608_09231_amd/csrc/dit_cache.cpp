@@ -141,6 +141,9 @@ struct dit_cache {
   std::vector<hipEvent_t> ev_pool;
   size_t ev_used = 0;
   std::vector<Pending> pending;
+  // end event of the last timed scope: the next scope starts from it unless
+  // the host has waited in between (then the GPU may have idled)
+  hipEvent_t ev_chain = nullptr;
 };
 
 namespace {
@@ -171,7 +174,8 @@ inline size_t rup(size_t x, size_t a) { return (x + a - 1) / a * a; }
 hipEvent_t next_event(dit_cache* c) {
   if (c->ev_used == c->ev_pool.size()) {
     hipEvent_t e;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    // timing only: no system-scope release / acquire around the timestamps
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     c->ev_pool.push_back(e);
   }
   return c->ev_pool[c->ev_used++];
@@ -182,10 +186,16 @@ struct Scope {
   int cls;
   double work;
   hipEvent_t a = nullptr;
+  // Back-to-back scopes share their boundary event (one timestamp per kernel
+  // class launch instead of two); a scope's span then also holds the launch
+  // gap before its first kernel.
   Scope(dit_cache* c_, int cls_, double work_) : c(c_), cls(cls_), work(work_) {
     if (c->prof) {
-      a = next_event(c);
-      if (a) hipEventRecord(a, c->stream);
+      a = c->ev_chain;
+      if (!a) {
+        a = next_event(c);
+        if (a) hipEventRecord(a, c->stream);
+      }
     }
   }
   ~Scope() {
@@ -195,9 +205,13 @@ struct Scope {
         hipEventRecord(b, c->stream);
         c->pending.push_back({cls, work, a, b});
       }
+      c->ev_chain = b;
     }
   }
 };
+
+// The host is about to wait for the GPU: the next timed scope starts afresh.
+void break_chain(dit_cache* c) { c->ev_chain = nullptr; }
 
 void collect_events(dit_cache* c) {
   if (!c->prof) return;
@@ -212,6 +226,7 @@ void collect_events(dit_cache* c) {
   }
   c->pending.clear();
   c->ev_used = 0;
+  c->ev_chain = nullptr;
 }
 
 // ---------------------------------------------------------------- helpers
@@ -1137,6 +1152,7 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
     if (t > 0) {
       HIPCK(hipEventRecord(c->ev_sums, c->stream));
       HIPCK(hipEventSynchronize(c->ev_sums));
+      break_chain(c);
     }
     const auto h0 = std::chrono::steady_clock::now();
     comp.clear();
