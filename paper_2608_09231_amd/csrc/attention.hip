@@ -375,15 +375,6 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_pipe_kernel(
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], oacc[dt], 0, 0, 0);
       }
   };
-  // wait until tile u has landed: tiles issued after it may stay in flight
-  auto wait_tile = [&](int u, int issued) {  // issued = tiles issued so far (0..issued-1)
-    const int later = issued - 1 - u;
-    if (later >= 2) __builtin_amdgcn_s_waitcnt((2 * 2 * CPW) | (7 << 4) | (0 << 8));
-    else if (later == 1) __builtin_amdgcn_s_waitcnt((2 * CPW) | (7 << 4) | (0 << 8));
-    else __builtin_amdgcn_s_waitcnt(0);
-    asm volatile("s_barrier" ::: "memory");
-  };
-
   const int ntiles = (Lk + KT - 1) / KT;
   f32x16_t s_cur[2], s_nxt[2];
   bf16x8_t p_prv[4], p_cur[4];
