@@ -693,13 +693,16 @@ __device__ __forceinline__ void wait_vmcnt_lgkm0() {
 __device__ __forceinline__ void barrier_no_fence() { asm volatile("s_barrier" ::: "memory"); }
 
 // 256 x 256 tiles, 8 waves of 64 x 128, BK = 64, with the whole 160 KB of
-// LDS as a ring of five 32 KB operand slices: operand i (A slice s = 2s,
-// W slice s = 2s + 1) lives in unit i % 5.  When slice kt starts, the units
-// of slice kt-1 are free and receive W slice kt+1 and A slice kt+2, so A
-// slices are copied two slices ahead of use and W slices one ahead, and the
-// end-of-slice wait leaves the A copies in flight.  The substep schedule is
-// the one of the two-stage kernel above (fragments double-buffered in
-// registers, LDS reads of the next substep between the MFMAs).
+// LDS as a ring of five 32 KB operand slices: operand i (W slice s = 2s,
+// A slice s = 2s + 1) lives in unit i % 5.  When slice kt starts, the units
+// of slice kt-1 are free and receive A slice kt+1 and W slice kt+2, so W
+// slices are copied two slices ahead of use and A slices one ahead, and the
+// end-of-slice wait leaves the W copies in flight.  The weights lead: they
+// come cold from HBM, while A was mostly written just before (about 3%
+// faster over the block-stack shapes than A leading; same result bits).
+// The substep schedule is the one of the two-stage kernel above (fragments
+// double-buffered in registers, LDS reads of the next substep between the
+// MFMAs).
 // Requires K % 64 == 0, K >= 128 and the LDS-staged epilogue's conditions.
 template <int KIND>
 __global__ __launch_bounds__(512) void gemm_bf16_ring_kernel(Batch b) {
@@ -744,20 +747,20 @@ __global__ __launch_bounds__(512) void gemm_bf16_ring_kernel(Batch b) {
   }
   auto unit = [&](int op) { return smem + (op % 5) * UNIT; };
   auto issue_a = [&](int s) {
-    char* d = unit(2 * s);
+    char* d = unit(2 * s + 1);
     const uint32_t so = (uint32_t)s * BK_ * 2;
 #pragma unroll
     for (int j = 0; j < INS; ++j) buf_lds16(P.A, (lds_void_t*)(d + (wave * INS + j) * 1024), aoff[j], so);
   };
   auto issue_w = [&](int s) {
-    char* d = unit(2 * s + 1);
+    char* d = unit(2 * s);
     const uint32_t so = (uint32_t)s * BK_ * 2;
 #pragma unroll
     for (int j = 0; j < INS; ++j) buf_lds16(P.W, (lds_void_t*)(d + (wave * INS + j) * 1024), boff[j], so);
   };
   auto rd = [&](int kt, int s, bf16x8_t(&af)[TM], bf16x8_t(&bfr)[TN]) {
-    const char* sA = unit(2 * kt);
-    const char* sB = unit(2 * kt + 1);
+    const char* sA = unit(2 * kt + 1);
+    const char* sB = unit(2 * kt);
     const int kc = 2 * s + lhalf;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
@@ -804,26 +807,26 @@ __global__ __launch_bounds__(512) void gemm_bf16_ring_kernel(Batch b) {
 
   const int nk = P.K / BK_;  // >= 2
   bf16x8_t a0[TM], b0[TN], a1[TM], b1[TN];
-  issue_a(0);
   issue_w(0);
-  issue_a(1);
-  wait_vmcnt_lgkm0<INS>();  // slice 0 has landed; A slice 1 may be in flight
+  issue_a(0);
+  issue_w(1);
+  wait_vmcnt_lgkm0<INS>();  // slice 0 has landed; W slice 1 may be in flight
   barrier_no_fence();
   rd(0, 0, a0, b0);
-  // slice kt with W slice kt+1 (HW) and A slice kt+2 (HA) copied meanwhile
-  auto slice = [&](int kt, auto hw, auto ha) {
-    constexpr bool HW = decltype(hw)::value, HA = decltype(ha)::value;
-    if constexpr (HW) issue_w(kt + 1);
+  // slice kt with A slice kt+1 (H1) and W slice kt+2 (H2) copied meanwhile
+  auto slice = [&](int kt, auto h1, auto h2) {
+    constexpr bool H1 = decltype(h1)::value, H2 = decltype(h2)::value;
+    if constexpr (H1) issue_a(kt + 1);
     rd(kt, 1, a1, b1); mm(a0, b0);
-    if constexpr (HW) sched(copy_t{}); else sched(nocopy_t{});
-    if constexpr (HA) issue_a(kt + 2);
+    if constexpr (H1) sched(copy_t{}); else sched(nocopy_t{});
+    if constexpr (H2) issue_w(kt + 2);
     rd(kt, 2, a0, b0); mm(a1, b1);
-    if constexpr (HA) sched(copy_t{}); else sched(nocopy_t{});
+    if constexpr (H2) sched(copy_t{}); else sched(nocopy_t{});
     rd(kt, 3, a1, b1); mm(a0, b0); sched(nocopy_t{});
     mm(a1, b1);
-    // slice kt+1 has landed (A slice kt+2 may still be in flight) and every
+    // slice kt+1 has landed (W slice kt+2 may still be in flight) and every
     // LDS read of slice kt has returned, so after the barrier its units are free
-    if constexpr (HA) wait_vmcnt_lgkm0<INS>();
+    if constexpr (H2) wait_vmcnt_lgkm0<INS>();
     else __builtin_amdgcn_s_waitcnt(0);
     barrier_no_fence();
   };
