@@ -269,6 +269,15 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
 // with the softmax of tile t (VALU), which depends on neither.  Five LDS
 // stages: tiles t-1 (V), t, t+1 (K), t+2 and t+3 (in flight).
 constexpr int PSTAGE = 5;
+
+// Work-groups are dispatched to the 8 XCDs round-robin (block b to XCD
+// b % 8); this maps block b to position x q + min(x, r) + b / 8 of n, so
+// that XCD x runs one contiguous range of positions.
+__device__ __forceinline__ int xcd_order(int b, int n) {
+  const int x = b & 7, q = n >> 3, r = n & 7;
+  return x * q + (x < r ? x : r) + (b >> 3);
+}
+
 template <int NW>
 __global__ __launch_bounds__(64 * NW) void flash_attn_pipe_kernel(
     const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restrict__ k, int64_t ldk,
@@ -276,14 +285,19 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_pipe_kernel(
     float scale_log2, SeqMap sm) {
   __shared__ __attribute__((aligned(1024))) char smem[PSTAGE][TILE_BYTES];  // [stage][K | V^T]
   const RowMap rm = sm.at(blockIdx.z);
-  vt += (int64_t)blockIdx.z * gridDim.y * D * ldvt;
 
   constexpr int QB = NW * 32;
   constexpr int CPW = 16 / NW;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lrow = lane & 31, lhalf = lane >> 5;
-  const int h = blockIdx.y;
-  const int q0 = blockIdx.x * QB + wave * 32;
+  // grid.x runs over (head, query block), head-major, and each XCD takes a
+  // contiguous range of it: the work-groups that read one head's K and V
+  // share an L2
+  const int nqb = (Lq + QB - 1) / QB;
+  const int lt = xcd_order(blockIdx.x, gridDim.x);
+  const int h = lt / nqb;
+  const int q0 = (lt % nqb) * QB + wave * 32;
+  vt += (int64_t)blockIdx.z * (gridDim.x / nqb) * D * ldvt;
 
   bf16x8_t qf[8];
   {
@@ -538,8 +552,9 @@ hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int
     return !(e && std::string(e) == "base");
   }();
   if (bounded_logits && pipe)
-    hipLaunchKernelGGL((flash_attn_pipe_kernel<kNW>), grid, dim3(64 * kNW), 0, s, (const bf16_t*)q, ldq,
-                       (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o, ldo, Lq, Lk, scale_log2, sm);
+    hipLaunchKernelGGL((flash_attn_pipe_kernel<kNW>), dim3(grid.x * heads, 1, nseq), dim3(64 * kNW), 0, s,
+                       (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o, ldo, Lq,
+                       Lk, scale_log2, sm);
   else if (bounded_logits)
     hipLaunchKernelGGL((flash_attn_bf16_kernel<true, kQG, kNW>), grid, dim3(64 * kNW), 0, s,
                        (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o,
