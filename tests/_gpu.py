@@ -62,6 +62,53 @@ def run_sampler(torch, w: synth.Workload, weights, x0, text, gate, *, T=None, B=
     return lat.cpu().numpy().astype(np.float64), sched, h
 
 
+def gate_lipschitz(g):
+    """Upper bound on |z(f) - z(f')| / |f - f'|_2 for a parsed oracle gate:
+    the product of the layers' spectral norms (ReLU is 1-Lipschitz), times
+    max 1/sd under z-scoring; parallel branches read disjoint inputs, so
+    their concatenation is bounded by the largest branch bound."""
+    def net(layers):
+        L = 1.0
+        for W, _ in layers:
+            L *= float(np.linalg.norm(W, 2))
+        return L
+    L = net(g.layers)
+    if g.branches:
+        L *= max(net(layers) for _, layers in g.branches)
+    if g.sd is not None:
+        L *= float(np.max(1.0 / np.abs(g.sd)))
+    return L
+
+
+def check_logits(sched, ores, gate_blob, f32_bound=None):
+    """The gate's logit at every unforced-or-forced step t >= 1.
+
+    (a) The host gate is Eq. 1's network: the oracle's gate evaluated on the
+        device's own recorded features reproduces the device's logit up to
+        the float32 storage of the logit.
+    (b) Against the oracle's replay: |z_dev - z_ref| is at most the gate's
+        Lipschitz bound times the distance of the two feature vectors (both
+        sides evaluate the same network), plus the float32 storage; with
+        ``f32_bound`` also at most f32_bound (1 + |z|).
+    Returns the largest |z_dev - z_ref|."""
+    from oracle import parse_gate_blob
+    g = parse_gate_blob(gate_blob)
+    L = gate_lipschitz(g)
+    worst = 0.0
+    for t in range(1, len(sched.full)):
+        z_dev = float(sched.logit[t])
+        z_own = g.logit(sched.features[t])
+        assert abs(z_dev - z_own) <= 1e-6 * (1.0 + abs(z_own)), (t, z_dev, z_own)
+        z_ref = float(ores.logit[t])
+        dz = abs(z_dev - z_ref)
+        df = float(np.linalg.norm(sched.features[t, :g.d_in] - ores.features[t, :g.d_in]))
+        assert dz <= L * df + 1e-6 * (1.0 + abs(z_ref)), (t, z_dev, z_ref, L, df)
+        if f32_bound is not None:
+            assert dz <= f32_bound * (1.0 + abs(z_ref)), (t, z_dev, z_ref)
+        worst = max(worst, dz)
+    return worst
+
+
 def check_schedule_against_oracle(sched, ores, margin=1e-3, cut=0.0):
     """Decisions agree wherever the decision statistic (gate logit, or q_t of
     the threshold rule) is more than `margin` from its cutoff `cut`; counts

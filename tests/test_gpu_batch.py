@@ -9,7 +9,7 @@ import pytest
 
 from oracle import sample as oracle_sample
 from paper_2608_09231_amd import binding, synth
-from tests._gpu import check_schedule_against_oracle, dev, rel_l2, torch_cuda
+from tests._gpu import check_logits, check_schedule_against_oracle, dev, rel_l2, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -52,13 +52,14 @@ def run_one(torch, h, w, x0, text, gate, T, B, **kw):
     return lat.cpu().numpy().astype(np.float64), sched
 
 
-def check_batch(name, S, *, masks=None, solver="euler", T=None, B=None):
+def check_batch(name, S, *, masks=None, solver="euler", T=None, B=None, gate=None):
     torch = torch_cuda()
     w = synth.workload(name)
     cfg = w.model
     T = T or w.T
     B = B or w.B
-    weights, x0, text, gate = inputs(w, S)
+    weights, x0, text, wgate = inputs(w, S)
+    gate = wgate if gate is None else gate
     h = binding.DitCache(cfg, weights.blob)
     try:
         xb, scheds = run_batch(torch, h, w, x0, text, gate, T, B, forced_masks=masks, solver=solver)
@@ -74,6 +75,7 @@ def check_batch(name, S, *, masks=None, solver="euler", T=None, B=None):
                              guidance=w.guidance, forced_mask=s.full, solver=solver)
         if masks is None:
             check_schedule_against_oracle(s, ores)
+        check_logits(s, ores, gate, 1e-5 if cfg.dtype == "f32" else None)
         err = rel_l2(xb[j], ores.x)
         assert err <= TOL[cfg.dtype], (j, err)
         xs, ss = singles[j]
@@ -91,6 +93,15 @@ def test_batch_replay_masks(name):
 @pytest.mark.parametrize("name", ["small_bf16", "small_seg_bf16", "small_cfg_bf16"])
 def test_batch_gated(name):
     check_batch(name, 3)
+
+
+def test_batch_flip_gate():
+    """A gate whose vote changes sign within a run: each prompt's lane paces
+    its own budget, so the prompts' schedules are checked one by one."""
+    from tests.test_gpu_sampler import FLIP, flip_gate
+    case = FLIP["cases"]["small_bf16_833"]
+    scheds = check_batch("small_bf16", 3, gate=flip_gate(case), T=case["T"], B=case["B"])
+    print("flip-gate batch schedules", [s.full.tolist() for s in scheds])
 
 
 def test_batch_unipc():

@@ -20,7 +20,7 @@ from oracle import dit, sample as oracle_sample, sigma_schedule
 from oracle.numerics import round_bf16, round_f32, storage_to_f64
 from oracle.sampler import rel_l1_sums
 from paper_2608_09231_amd import binding, synth
-from tests._gpu import check_schedule_against_oracle, dev, host_bf16, rel_l2, run_sampler, torch_cuda
+from tests._gpu import check_logits, check_schedule_against_oracle, dev, host_bf16, rel_l2, run_sampler, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -42,6 +42,7 @@ def reduced_parity(name, T, B, **kw):
                          guidance=w.guidance, forced_mask=sched.full)
     say(f"{w.name}: oracle done ({time.time() - t0:.1f} s)")
     check_schedule_against_oracle(sched, ores)
+    check_logits(sched, ores, gate)
     err = rel_l2(x_gpu, ores.x)
     say(f"{w.name}: latent rel-L2 {err:.3e}")
     assert err <= 2e-2
@@ -66,6 +67,7 @@ def test_wan_width_one_block_reduced_tokens():
     h.close()
     ores = oracle_sample(m, weights.tensors, gate, x0, text, 3, 2, shift=ww.shift, forced_mask=sched.full)
     check_schedule_against_oracle(sched, ores)
+    check_logits(sched, ores, gate)
     err = rel_l2(x_gpu, ores.x)
     say(f"wan width: latent rel-L2 {err:.3e}")
     assert err <= 2e-2

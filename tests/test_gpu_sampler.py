@@ -12,16 +12,18 @@ import pytest
 
 from oracle import sample as oracle_sample
 from paper_2608_09231_amd import binding, synth
-from tests._gpu import check_schedule_against_oracle, rel_l2, run_sampler, torch_cuda
+from tests._gpu import check_logits, check_schedule_against_oracle, rel_l2, run_sampler, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
 TOL = {"f32": 1e-5, "bf16": 2e-2}
 SUM_TOL = {"f32": 1e-5, "bf16": 1e-3}
+# f32 runs: the device logit within 1e-5 (1 + |z|) of the oracle's
+LOGIT_F32 = 1e-5
 
 
 def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5, gate=None, policy="gate", delta=0.0,
-           solver="euler"):
+           solver="euler", expect_schedule=None):
     torch = torch_cuda()
     w = synth.workload(name)
     cfg = w.model
@@ -54,11 +56,20 @@ def parity(name, *, T=None, B=None, indicator="modulated", tau=0.5, gate=None, p
         assert np.all(np.abs(got[ok][:, d] - ref[ok][:, d]) <= SUM_TOL[cfg.dtype] * ref[ok][:, mcol]), (d, got, ref)
     np.testing.assert_allclose(sched.features[1:, :4], ores.features[1:, :4], rtol=1e-12)
     np.testing.assert_allclose(sched.features[1:, 4:], ores.features[1:, 4:], rtol=10 * SUM_TOL[cfg.dtype])
+    if policy == "gate":
+        dz = check_logits(sched, ores, gate, LOGIT_F32 if cfg.dtype == "f32" else None)
+        print(f"{name}: largest |z_dev - z_oracle| {dz:.2e}")
+    elif policy == "threshold":
+        # q_t is feature f7 itself
+        np.testing.assert_array_equal(sched.logit[1:], sched.features[1:, 7].astype(np.float32))
     gated = oracle_sample(cfg, weights.tensors, gate, x0, text, T, B, shift=w.shift, tau=tau,
                           guidance=w.guidance, indicator=indicator, **pol)
     stat = ores.logit[1:] - (delta if policy == "threshold" else 0.0)
     if np.all(np.isnan(stat) | (np.abs(stat) > (1e-2 * abs(delta) if policy == "threshold" else 1e-3))):
         np.testing.assert_array_equal(sched.full, gated.full)
+    if expect_schedule is not None:
+        np.testing.assert_array_equal(gated.full, expect_schedule)
+        np.testing.assert_array_equal(sched.full, expect_schedule)
     return sched, ores, err
 
 
@@ -112,6 +123,51 @@ def test_wan_branched_gate():
     gate = synth.make_branched_gate_blob(seed=5, zscore=(mu, sd))
     parity("tiny", gate=gate)
     parity("small_cross_bf16", gate=gate)
+
+
+def _flip_cases():
+    import json
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "flip_gates.json")
+    with open(path) as f:
+        data = json.load(f)
+    return data
+
+
+FLIP = _flip_cases()
+
+
+def flip_gate(case):
+    """The seeded gate of the case's shape with its output bias moved by beta
+    (tests/golden/make_flip_gates.py chose beta with the oracle alone)."""
+    z = (np.array(FLIP["zscore_mu"], np.float32), np.array(FLIP["zscore_sd"], np.float32))
+    kind, seed, std = case["gate"], case["gate_seed"], case["gate_std"]
+    if kind == "833":
+        g = synth.make_gate_blob((8, 32, 16, 1), seed=seed, std=std)
+    elif kind == "449z":
+        g = synth.make_gate_blob((6, 8, 8, 32, 1), seed=seed, std=std, zscore=z)
+    else:
+        g = synth.make_branched_gate_blob(seed=seed, std=std, zscore=z)
+    g[-1] = np.float32(g[-1] + np.float32(case["beta"]))
+    return g
+
+
+@pytest.mark.parametrize("cid", sorted(FLIP["cases"]))
+def test_gate_vote_changes_sign(cid):
+    """Alg. 2 driven by the gate itself: unforced steps vote compute and
+    unforced steps vote reuse within one run, so the schedule is neither of
+    the two closed forms a one-signed gate yields.  Device, the oracle's own
+    gated run and the stored schedule agree bit for bit (every unforced
+    logit is far from the threshold), and the logits agree by value."""
+    case = FLIP["cases"][cid]
+    T, B = case["T"], case["B"]
+    sched, ores, err = parity(case["workload"], T=T, B=B, gate=flip_gate(case), expect_schedule=case["schedule"])
+    closed = [np.r_[np.ones(B), np.zeros(T - B)], np.r_[1, np.zeros(T - B), np.ones(B - 1)]]
+    assert not any(np.array_equal(sched.full, c) for c in closed)
+    unforced = [t for t in range(1, T) if not sched.forced[t]]
+    z = sched.logit[unforced]
+    assert np.any(z > 0) and np.any(z < 0)
+    print(cid, "schedule", sched.full.tolist(), "rel-L2", err)
 
 
 def test_static_policy():
