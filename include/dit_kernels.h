@@ -78,6 +78,28 @@ dit_status dit_attention_bf16(const void* q, int64_t ldq, const void* k, int64_t
                               int32_t Lq, int32_t Lk, int32_t heads, int32_t flags, void* vt_ws,
                               void* hip_stream);
 
+/* Largest v-transpose the allocation-free attention holds: heads * 128 *
+ * round_up(Lk, 64) bf16 elements (32 MiB; e.g. 24 heads at up to 5440 keys). */
+#define DIT_NOALLOC_VT_MAX_ELEMS (16 * 1024 * 1024)
+
+/* dit_attention_bf16 without the vt_ws workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  The transposed values go to a
+ * fixed device array of DIT_NOALLOC_VT_MAX_ELEMS bf16 elements inside the
+ * library, one per GPU, held until the process ends; the call allocates
+ * nothing (no hipMalloc / hipFree, no allocating library routine).  The
+ * array's device address is looked up once per device, on the first call
+ * made with that device current.  Same arguments, kernels and result bits
+ * as dit_attention_bf16.  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (other streams or host threads) race and
+ * must be serialised by the caller.  Errors: as dit_attention_bf16, plus
+ * DIT_ESHAPE when heads * 128 * round_up(Lk, 64) > DIT_NOALLOC_VT_MAX_ELEMS
+ * (nothing is launched). */
+dit_status dit_attention_bf16_noalloc(const void* q, int64_t ldq, const void* k, int64_t ldk,
+                                      const void* v, int64_t ldv, void* o, int64_t ldo,
+                                      int32_t Lq, int32_t Lk, int32_t heads, int32_t flags,
+                                      void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -32,7 +32,7 @@ K_CLASSES = ["gemm", "attn", "indicator", "reuse", "full_other", "once"]
 EXPORTS = ["dit_cache_create", "dit_cache_sample", "dit_cache_sample_ex", "dit_cache_sample_batch",
            "dit_cache_destroy",
            "dit_cache_last_error", "dit_cache_set_profiling", "dit_cache_get_stats",
-           "dit_cache_reset_stats", "dit_gemm_bf16", "dit_attention_bf16"]
+           "dit_cache_reset_stats", "dit_gemm_bf16", "dit_attention_bf16", "dit_attention_bf16_noalloc"]
 
 
 class ModelConfigC(C.Structure):
@@ -102,6 +102,8 @@ def load(path: str = LIB_PATH):
     lib.dit_gemm_bf16.argtypes = [C.POINTER(GemmDescC), vp]
     lib.dit_attention_bf16.argtypes = [vp, C.c_int64, vp, C.c_int64, vp, C.c_int64, vp, C.c_int64,
                                        C.c_int32, C.c_int32, C.c_int32, C.c_int32, vp, vp]
+    lib.dit_attention_bf16_noalloc.argtypes = [vp, C.c_int64, vp, C.c_int64, vp, C.c_int64, vp, C.c_int64,
+                                               C.c_int32, C.c_int32, C.c_int32, C.c_int32, vp]
     for n in EXPORTS:
         f = getattr(lib, n)
         if n not in ("dit_cache_destroy", "dit_cache_last_error"):
@@ -283,4 +285,16 @@ def attention_bf16(q, k, v, o, *, Lq, Lk, heads, ldq, ldk, ldv, ldo, vt_ws, flag
     lib = load()
     st = lib.dit_attention_bf16(q.data_ptr(), ldq, k.data_ptr(), ldk, v.data_ptr(), ldv,
                                 o.data_ptr(), ldo, Lq, Lk, heads, flags, vt_ws.data_ptr(), _stream_ptr(stream))
+    _check(st, None)
+
+
+NOALLOC_VT_MAX_ELEMS = 16 * 1024 * 1024
+
+
+def attention_bf16_noalloc(q, k, v, o, *, Lq, Lk, heads, ldq, ldk, ldv, ldo, flags=0, stream=None):
+    """dit_attention_bf16_noalloc: the library's own device array holds the
+    transposed values (no workspace argument, nothing allocated)."""
+    lib = load()
+    st = lib.dit_attention_bf16_noalloc(q.data_ptr(), ldq, k.data_ptr(), ldk, v.data_ptr(), ldv,
+                                        o.data_ptr(), ldo, Lq, Lk, heads, flags, _stream_ptr(stream))
     _check(st, None)

@@ -13,6 +13,7 @@
 
 #include <chrono>
 #include <cmath>
+#include <mutex>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -1513,3 +1514,56 @@ dit_status dit_attention_bf16(const void* q, int64_t ldq, const void* k, int64_t
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------- allocation-free attention
+// Transposed values of dit_attention_bf16_noalloc.  In host code `scratch`
+// names a host-side stand-in, not device memory: kernels and copies take
+// the address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) uint16_t scratch[DIT_NOALLOC_VT_MAX_ELEMS];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up once per device.
+dit_status scratch_ptr(void** out) {
+  dit_cache* c = nullptr;
+  int dev = -1;
+  HIPCK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(c, DIT_EINVAL, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIPCK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(c, DIT_EHIP, "hipGetSymbolAddress returned no address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return DIT_OK;
+}
+}  // namespace
+
+extern "C" dit_status dit_attention_bf16_noalloc(const void* q, int64_t ldq, const void* k, int64_t ldk,
+                                                 const void* v, int64_t ldv, void* o, int64_t ldo, int32_t Lq,
+                                                 int32_t Lk, int32_t heads, int32_t flags, void* hip_stream) {
+  dit_cache* c = nullptr;
+  if (!q || !k || !v || !o) return fail(c, DIT_EINVAL, "null argument");
+  if (Lq < 1 || Lk < 1 || heads < 1) return fail(c, DIT_ESHAPE, "bad attention shape");
+  if (flags & ~DIT_ATTN_BOUNDED_LOGITS) return fail(c, DIT_EINVAL, "bad attention flags");
+  if (ldq < heads * 128 || ldk < heads * 128 || ldv < heads * 128 || ldo < heads * 128)
+    return fail(c, DIT_ESHAPE, "row stride smaller than heads*128");
+  const size_t need = (size_t)heads * 128 * rup((size_t)Lk, 64);
+  if (need > (size_t)DIT_NOALLOC_VT_MAX_ELEMS)
+    return fail(c, DIT_ESHAPE, "heads * 128 * round_up(Lk, 64) = " + std::to_string(need) +
+                                   " exceeds the allocation-free limit of " +
+                                   std::to_string((size_t)DIT_NOALLOC_VT_MAX_ELEMS) + " elements");
+  void* vt = nullptr;
+  TRY(scratch_ptr(&vt));
+  hipStream_t s = (hipStream_t)hip_stream;
+  HIPCK(dit::launch_transpose_v_bf16(v, ldv, vt, Lk, heads, s));
+  HIPCK(dit::launch_flash_attn_bf16(q, ldq, k, ldk, vt, (int)rup(Lk, 64), o, ldo, Lq, Lk, heads,
+                                    (flags & DIT_ATTN_BOUNDED_LOGITS) != 0, s));
+  HIPCK(hipStreamSynchronize(s));
+  return DIT_OK;
+}

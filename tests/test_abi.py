@@ -76,3 +76,16 @@ def test_blob_size_matches_layout():
         st, msg = _create(binding.model_config_c(cfg), blob)
         assert st == binding.DIT_ESHAPE
         assert msg.endswith(str(n * (2 if cfg.dtype == "bf16" else 4))), (name, msg)
+
+
+def test_noalloc_attention_rejects_oversized_on_the_host():
+    """The size check of the allocation-free attention runs before any
+    device call (no GPU needed; nothing is launched)."""
+    lib = binding.load()
+    fake = C.c_void_p(0x1000)
+    H = 24 * 128
+    st = lib.dit_attention_bf16_noalloc(fake, H, fake, H, fake, H, fake, H, 8, 5441, 24, 0, None)
+    assert st == binding.DIT_ESHAPE
+    assert "allocation-free limit" in lib.dit_cache_last_error(None).decode()
+    st = lib.dit_attention_bf16_noalloc(None, H, fake, H, fake, H, fake, H, 8, 8, 24, 0, None)
+    assert st == binding.DIT_EINVAL
