@@ -1,18 +1,23 @@
 #!/usr/bin/env python3
-"""Benchmark: budget-aware cached sampling of the FLUX.1-dev-shaped MMDiT
-(19 double + 38 single blocks, H 3072, 24 x 128 heads, 4096 image + 512 text
-tokens, bf16, random init), T = 28 Euler steps at budget B = 10, on one
-MI355X.
+"""Benchmark: budget-aware cached sampling on one MI355X.
+
+Default workload: the Wan2.1-14B-shaped video DiT (40 blocks, H 5120, 40 x
+128 heads, FFN 13824, 32760 video tokens + 512 text tokens, bf16, random
+init), T = 50 UniPC steps at budget B = 12 -- the largest single-GPU
+workload.  ``--workload flux1024`` (and flux2048, qwen_cfg, ...) runs the
+others with the same kernels.
 
 One bench step = one whole sample (T denoising steps: B full evaluations and
 T - B residual reuses, gate decisions included).  `value` is denoising
 steps per second (T / seconds per sample) with all inputs resident in HBM;
 samples/s is reported beside it.  The roofline object covers the dominant
-kernel class (the block-stack GEMMs), timed live with HIP events on the
-sampler's stream during the timed samples: achieved = algorithmic GEMM
-FLOPs (2 M N K per launch) / summed GEMM event time.
+kernel class of the workload (the one with the most time: attention for
+Wan, the block-stack GEMMs for FLUX-1024), timed live with HIP events on the
+sampler's stream during the timed samples: achieved = algorithmic FLOPs of
+the class (2 M N K per GEMM, 4 Lq Lk H per attention) / its summed event
+time, which is the algorithmic FLOPs per launch over the average launch.
 
-    python bench.py [--gpus 1] [--steps 3] [--warmup 1] [--workload flux1024]
+    python bench.py [--gpus 1] [--steps 3] [--warmup 1] [--workload wan14b]
 """
 import argparse
 import json
@@ -33,9 +38,19 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(w, budget_s=40.0):
+def cpu_baseline(w, rows=1024, q_sample=128):
     """Time the CPU oracle (as it stands) on a bounded sample of the same
-    workload and extrapolate to one whole sample."""
+    workload and extrapolate to one whole sample.
+
+    Per block kind, the oracle's block runs once at `rows` image tokens (all
+    text tokens, full width); its attention runs once for `q_sample` query
+    rows against the full key count.  The attention time per query-key pair
+    (beta) separates the block's time into a part linear in the sequence
+    length L (alpha L) and self-attention (beta L^2), which extrapolate to
+    the full L.  The per-step pass (embed, indicator, final layer, step
+    rule) runs on the same `rows` tokens and scales with the token count; the
+    modulation table is timed on the 1-block model and scaled by the
+    modulation width."""
     import dataclasses
 
     from oracle import dit
@@ -44,6 +59,7 @@ def cpu_baseline(w, budget_s=40.0):
     from paper_2608_09231_amd import synth
 
     cfg = w.model
+    n_s = min(rows, cfg.n_img)
     small = dataclasses.replace(cfg, n_double=min(1, cfg.n_double), n_single=min(1, cfg.n_single),
                                 n_cross=min(1, cfg.n_cross), name=cfg.name + "_1blk")
     weights = synth.make_weights(small, w.seed)
@@ -56,7 +72,7 @@ def cpu_baseline(w, budget_s=40.0):
     txt = dit.text_in(P, t64)
     mods = dit.mod_table(P, dit.vec_table(P, sig[:w.T], t64))
     t_once = (time.perf_counter() - t0) * cfg.n_mod / small.n_mod
-    x = round_f32(x0.astype(np.float64))
+    x = round_f32(x0[:n_s].astype(np.float64))
     mod = mods[0]
     t0 = time.perf_counter()
     h = dit.patch_embed(P, x)
@@ -67,25 +83,41 @@ def cpu_baseline(w, budget_s=40.0):
     h_out = P.rs(h + h)
     v = dit.final_layer(P, h_out, mod)
     x = round_f32(x + 0.01 * v)
-    t_common = time.perf_counter() - t0
+    t_common = (time.perf_counter() - t0) * cfg.n_img / n_s
+
+    # attention time per query-key pair, full key count
+    joint = cfg.n_cross == 0
+    L_full = cfg.n_img + (cfg.n_txt if joint else 0)
+    L_s = n_s + (cfg.n_txt if joint else 0)
+    rng = np.random.default_rng(0)
+    qs = P.rs(rng.standard_normal((q_sample, cfg.hidden)))
+    kv = P.rs(rng.standard_normal((L_full, cfg.hidden)))
+    t0 = time.perf_counter()
+    dit.attention(qs, kv, kv, cfg.heads, cfg.head_dim)
+    beta = (time.perf_counter() - t0) / (q_sample * L_full)
+
+    hs = h
     t_blocks = 0.0
-    if cfg.n_double:
+    parts = []
+    for kind, count in (("double", cfg.n_double), ("single", cfg.n_single), ("cross", cfg.n_cross)):
+        if not count:
+            continue
         t0 = time.perf_counter()
-        s_img, s_txt = dit.double_block(P, 0, h, txt, mod)
-        t_blocks += (time.perf_counter() - t0) * cfg.n_double
-    if cfg.n_single:
-        xj = np.concatenate([txt, h])
-        t0 = time.perf_counter()
-        dit.single_block(P, 0, xj, mod)
-        t_blocks += (time.perf_counter() - t0) * cfg.n_single
-    if cfg.n_cross:
-        t0 = time.perf_counter()
-        dit.cross_block(P, 0, h, txt, mod)
-        t_blocks += (time.perf_counter() - t0) * cfg.n_cross
+        if kind == "double":
+            dit.double_block(P, 0, hs, txt, mod)
+        elif kind == "single":
+            dit.single_block(P, 0, np.concatenate([txt, hs]), mod)
+        else:
+            dit.cross_block(P, 0, hs, txt, mod)
+        t_s = time.perf_counter() - t0
+        alpha = max(t_s - beta * L_s * L_s, 0.0) / L_s
+        t_full = alpha * L_full + beta * L_full * L_full
+        t_blocks += t_full * count
+        parts.append(f"{kind} {t_s:.2f} s at {L_s} rows -> {t_full:.1f} s at {L_full}")
     nb = cfg.batch
-    t_full = t_common + nb * t_blocks
+    t_step_full = t_common + nb * t_blocks
     t_reuse = t_common
-    t_sample = t_once + w.B * t_full + (w.T - w.B) * t_reuse
+    t_sample = t_once + w.B * t_step_full + (w.T - w.B) * t_reuse
     try:
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
@@ -96,24 +128,25 @@ def cpu_baseline(w, budget_s=40.0):
         "unit": "denoising steps/s",
         "cores": min(cores, threads),
         "kind": "oracle",
-        "sample": (f"float64 NumPy oracle timed on one block of each kind of the {cfg.name} model at full "
-                   f"width and token count, one per-step pass (embed, indicator, final layer, Euler) "
-                   f"and the modulation table of the 1-block model; extrapolated to "
-                   f"{cfg.n_double}+{cfg.n_single}+{cfg.n_cross} blocks, T={w.T}, B={w.B}: "
-                   f"{t_sample:.1f} s per sample (block time {t_blocks:.1f} s per full step)"),
+        "sample": (f"float64 NumPy oracle, extrapolated: one block of each kind of the {cfg.name} model at "
+                   f"full width on {n_s} image tokens ({'; '.join(parts)}), its attention on {q_sample} "
+                   f"queries x {L_full} keys (time per query-key pair {beta * 1e9:.2f} ns), one "
+                   f"per-step pass on the same tokens and the 1-block modulation table; to {cfg.n_double}+{cfg.n_single}+"
+                   f"{cfg.n_cross} blocks, T={w.T}, B={w.B}: {t_sample:.1f} s per sample"),
         "seconds_per_sample": t_sample,
     }
 
 
-def gemm_traffic(workload):
-    """HBM-side bytes per GEMM launch from the committed rocprofv3 counter
-    summary, or None when it does not cover this workload or the GEMM
-    source changed since the counters were taken."""
+def kernel_traffic(kernel, workload, source):
+    """HBM-side bytes per launch of `kernel` from the committed rocprofv3
+    counter summary profiles/<kernel>_<workload>_hbm_traffic.md, or None when
+    it does not cover this workload or `source` changed since the counters
+    were taken."""
     import hashlib
     import re
 
-    path = os.path.join(ROOT, "profiles", f"gemm_bf16_{workload}_hbm_traffic.md")
-    src = os.path.join(ROOT, "paper_2608_09231_amd", "csrc", "gemm_bf16.hip")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_hbm_traffic.md")
+    src = os.path.join(ROOT, "paper_2608_09231_amd", "csrc", source)
     try:
         txt = open(path).read()
         m = re.search(r"```json\n(.*?)\n```", txt, flags=re.S)
@@ -121,7 +154,7 @@ def gemm_traffic(workload):
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
     except (OSError, AttributeError, ValueError):
         return None
-    if data.get("gemm_source_sha256_16") != sha:
+    if data.get("source_sha256_16") != sha:
         return None
     return data["traffic_bytes_per_launch"]
 
@@ -180,10 +213,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="flux1024")
+    ap.add_argument("--workload", default="wan14b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="time without per-kernel events")
-    ap.add_argument("--prompts", type=int, default=4,
+    ap.add_argument("--prompts", type=int, default=0,
                     help="multi-prompt leg: this many prompts sampled together (0 or 1: skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 256 MiB device-to-device copy first (HBM counter calibration)")
@@ -252,7 +285,13 @@ def main():
     attn_tflops = work["attn"] / (ms["attn"] * 1e-3) / 1e12 if ms["attn"] else 0.0
     reuse_gbs = work["reuse"] / (ms["reuse"] * 1e-3) / 1e9 if ms["reuse"] else 0.0
     ind_gbs = work["indicator"] / (ms["indicator"] * 1e-3) / 1e9 if ms["indicator"] else 0.0
-    launches = max(st["launches"]["gemm"], 1)
+    # dominant kernel class: the MFMA class with the most event time
+    dom = "attn" if ms["attn"] > ms["gemm"] else "gemm"
+    dom_kernel = {"gemm": ("gemm_bf16_ring_kernel", "bf16 GEMM (block-stack linear layers)", "gemm_bf16.hip"),
+                  "attn": ("flash_attn_pipe_kernel", "bf16 flash attention (self- and cross-attention)",
+                           "attention.hip")}[dom]
+    launches = max(st["launches"][dom], 1)
+    dom_tflops = work[dom] / (ms[dom] * 1e-3) / 1e12 if ms[dom] else 0.0
     out = {
         "metric": "denoising steps/s at budget B/T",
         "value": w.T / (ms_per_sample * 1e-3),
@@ -268,22 +307,26 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic (seeded N(0,1) latent and text embeddings, N(0,0.02) random-init weights, N(0,0.3) gate)",
-        "config": {"workload": cfg.name, "T": w.T, "B": w.B, "solver": w.solver, "blocks": f"{cfg.n_double} double + {cfg.n_single} single",
+        "config": {"workload": cfg.name, "T": w.T, "B": w.B, "solver": w.solver,
+                   "blocks": (f"{cfg.n_cross} video (self-attn, cross-attn, FFN)" if cfg.n_cross
+                              else f"{cfg.n_double} double + {cfg.n_single} single"),
                    "hidden": cfg.hidden, "heads": cfg.heads, "img_tokens": cfg.n_img, "txt_tokens": cfg.n_txt,
-                   "batch": cfg.batch, "gate": "-".join(map(str, w.gate_widths))},
+                   "mlp_hidden": cfg.mlp_hidden, "batch": cfg.batch, "gate": "-".join(map(str, w.gate_widths))},
         "roofline": {
             "bound": "mfma",
-            "kernel": "bf16 GEMM (block-stack linear layers)",
-            "achieved": gemm_tflops,
+            "kernel": f"{dom_kernel[0]}: {dom_kernel[1]}",
+            "achieved": dom_tflops,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
-            "frac": gemm_tflops / PEAK_BF16_TFLOPS,
-            "traffic": gemm_traffic(cfg.name),
+            "frac": dom_tflops / PEAK_BF16_TFLOPS,
+            "traffic": kernel_traffic(dom_kernel[0], cfg.name, dom_kernel[2]),
             "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-            "avg_launch_us": ms["gemm"] * 1e3 / launches,
-            "flops_per_launch": work["gemm"] / launches,
+            "avg_launch_us": ms[dom] * 1e3 / launches,
+            "flops_per_launch": work[dom] / launches,
         },
         "kernels": {
+            "gemm_tflops": gemm_tflops,
+            "gemm_frac_bf16_peak": gemm_tflops / PEAK_BF16_TFLOPS,
             "attention_tflops": attn_tflops,
             "attention_frac_bf16_peak": attn_tflops / PEAK_BF16_TFLOPS,
             "reuse_path_gbs": reuse_gbs,
@@ -296,7 +339,9 @@ def main():
             "host_gate_ms_per_sample": st["host_gate_ms"] / max(args.steps, 1),
             "full_steps": st["full_steps"], "reuse_steps": st["reuse_steps"],
         },
-        "paper_context": "paper: FLUX.1-dev 1024^2, T=50, 31.13 s full compute, BAG B=9 5.99 s on one RTX 4090 (Tab. 1); not comparable hardware or T",
+        "paper_context": ("paper (one RTX 4090, precision not stated; context only): Wan2.1-T2V-1.3B 832x480, 65 "
+                          "frames, 50-step UniPC: 184.40 s full compute, BAG B=15 55.76 s (3.31x) (Tab. 2); "
+                          "FLUX.1-dev 1024^2, T=50: 31.13 s full, BAG B=9 5.99 s (Tab. 1)"),
     }
     if args.prompts > 1:
         out["multi_prompt"] = multi_prompt(h, w, lat0, args, ms_per_sample)
