@@ -78,9 +78,12 @@ struct Lane {
   void* txt = nullptr;      // [nb, Nt, H] projected text tokens
   float* x_last = nullptr;  // f32 [N, C]: UniPC's corrected sample of the previous step
   float* mh[3] = {};        // f32 [N, C]: UniPC data predictions (rotating)
+  float* xalt = nullptr;    // f32 [N, C]: second latent buffer (the reuse candidate's Euler result)
+  float* vspec = nullptr;   // f32 [N, C]: the reuse candidate's velocity (UniPC)
   int cnt = 0, t_last = 0, i_prev = -1, i_last = -1, i_new = 0;
   double acc = 0.0;
   bool dec = true;
+  bool spec = false;  // this step's fused launch formed a reuse candidate
 };
 
 struct dit_cache {
@@ -390,7 +393,8 @@ dit_status dalloc(dit_cache* c, P** p, size_t bytes) {
 }
 
 void free_lane(Lane& l) {
-  void* ps[] = {l.h, l.mbuf[0], l.mbuf[1], l.mbuf[2], l.r, l.txt, l.x_last, l.mh[0], l.mh[1], l.mh[2]};
+  void* ps[] = {l.h, l.mbuf[0], l.mbuf[1], l.mbuf[2], l.r, l.txt, l.x_last, l.mh[0], l.mh[1], l.mh[2],
+                l.xalt, l.vspec};
   for (void* p : ps)
     if (p) hipFree(p);
   l = Lane{};
@@ -405,6 +409,8 @@ dit_status alloc_lane(dit_cache* c, Lane& l) {
   TRY(dalloc(c, &l.txt, (size_t)c->nb * c->Nt * c->H * e));
   TRY(dalloc(c, &l.x_last, NC * 4));
   for (auto& m : l.mh) TRY(dalloc(c, &m, NC * 4));
+  TRY(dalloc(c, &l.xalt, NC * 4));
+  TRY(dalloc(c, &l.vspec, NC * 4));
   return DIT_OK;
 }
 
@@ -472,7 +478,8 @@ dit_status alloc_workspace(dit_cache* c) {
     std::vector<float> one(H, 1.f);
     HIPCK(hipMemcpy(c->ones, one.data(), H * 4, hipMemcpyHostToDevice));
   }
-  c->max_partials = std::max(dit::indicator_partials(N), dit::reuse_indicator_partials(N));
+  c->max_partials = std::max({dit::indicator_partials(N), dit::reuse_indicator_partials(N),
+                              dit::step_fused_partials(N, H, c->nb)});
   TRY(dalloc(c, &c->partials, (size_t)c->max_partials * 4 * sizeof(double)));
   HIPCK(hipEventCreateWithFlags(&c->ev_sums, hipEventDisableTiming));
   return ensure_lanes(c, 1);
@@ -1087,7 +1094,10 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
 
   const bool pair = nb == 2;
   const bool unipc = p.solver == DIT_SOLVER_UNIPC;
-  const bool fused = c->bf16 && dit::reuse_fused_fits(C, H);
+  // step: one fused launch per sample and step does the indicator and the
+  // reuse candidate (bf16, C = 64); fused: the older pair of fused kernels
+  const bool step = c->bf16 && dit::step_fused_fits(C, H, nb);
+  const bool fused = !step && c->bf16 && dit::reuse_fused_fits(C, H);
   const bool fused_euler = !pair && proj_fits(c) && !unipc;  // Euler folded into the projection
   const double thr = std::log(p.tau / (1.0 - p.tau));
   // mu(B, T) of the static policy: computed steps at floor(i T / B)
@@ -1103,7 +1113,15 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
   auto modxp = [&](int j, int b) {
     return c->modx ? c->modx + (size_t)mod_slot(c, j, b) * c->cfg.n_cross * T * 6 * H : nullptr;
   };
-  auto lat = [&](int j) { return latents + j * NC; };
+  // Each lane's current latent: the caller's buffer or the lane's second
+  // buffer, which trade places when a reused step takes the candidate's
+  // Euler result; the caller's buffer receives x_T at the end.
+  std::vector<float*> cur(S), alt(S);
+  for (int j = 0; j < S; ++j) {
+    cur[j] = latents + j * NC;
+    alt[j] = c->lanes[j].xalt;
+  }
+  auto lat = [&](int j) { return cur[j]; };
   auto fail_all = [&](int t, dit_status st, const std::string& m) {
     for (int j = 0; j < S; ++j) out[j].steps_done = t;
     return fail(c, st, m);
@@ -1127,7 +1145,23 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
       double* sums = c->sums_dev + 4 * j;
       const void* mp = t ? l.mbuf[l.i_prev] : nullptr;
       const void* ml = t ? l.mbuf[l.i_last] : nullptr;
-      if (fused) {
+      if (step) {
+        // a step known to compute (t = 0, replay mask, spend-the-remainder,
+        // static mask) writes h for the block stack instead of a reuse candidate
+        bool known_full = t == 0;
+        if (p.forced_mask) known_full = known_full || p.forced_mask[(size_t)j * T + t];
+        else if (p.policy == DIT_POLICY_GATE) known_full = known_full || B - l.cnt >= T - t;
+        else if (p.policy == DIT_POLICY_STATIC) known_full = known_full || mu[t];
+        l.spec = !known_full;
+        const int reads = t == 0 ? 0 : (l.i_prev == l.i_last ? 1 : 2);
+        Scope sc(c, DIT_K_INDICATOR, (double)NH * c->esz * (1 + reads + (l.spec ? nb : 0)));
+        const float* mf0 = modp(j, 0, t) + (c->n_mod - 2 * H);
+        const float* mf1 = pair ? modp(j, 1, t) + (c->n_mod - 2 * H) : nullptr;
+        HIPCK(dit::launch_step_fused(lat(j), C, c->M.img_in.w, c->M.img_in.b, l.mbuf[l.i_new], mp, ml, N, H, sh0, sc0,
+                                     t ? c->partials : nullptr, sums, l.spec ? l.r : nullptr, nb, c->M.fin.w,
+                                     c->M.fin.b, mf0, mf1, dsig, (float)p.guidance, unipc ? nullptr : alt[j],
+                                     unipc ? l.vspec : nullptr, l.spec ? nullptr : l.h, c->stream));
+      } else if (fused) {
         // embedding recomputed in LDS: reads m_{t-1} and m_{t_last} (once if equal), writes m_t
         Scope sc(c, DIT_K_INDICATOR, (double)NH * c->esz * (t == 0 ? 1 : (l.i_prev == l.i_last ? 2 : 3)));
         HIPCK(dit::launch_reuse_indicator(lat(j), C, c->M.img_in.w, c->M.img_in.b, l.mbuf[l.i_new], mp, ml, N, H,
@@ -1211,9 +1245,10 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
           std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - h0).count();
 
     // the step rule of sample j once its velocity (or velocities) are in vel
-    auto step_rule = [&](int j, bool vpair, bool folded) -> dit_status {
+    auto step_rule = [&](int j, bool vpair, bool folded, const float* vbuf = nullptr) -> dit_status {
       Lane& l = c->lanes[j];
       if (!unipc && folded) return DIT_OK;
+      if (!vbuf) vbuf = c->vel;
       Scope sc(c, l.dec ? DIT_K_FULL_OTHER : DIT_K_REUSE, 0);
       if (unipc) {
         // the guidance pair's two velocities are combined here unless the
@@ -1222,11 +1257,11 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
         float* m_t = l.mh[t % 3];
         const float* m_s = t >= 1 ? l.mh[(t + 2) % 3] : nullptr;
         const float* m_p = (t >= 2 && k.cp != 0.f) ? l.mh[(t + 1) % 3] : nullptr;
-        HIPCK(dit::launch_unipc(lat(j), c->vel, vpair ? c->vel + NC : nullptr, (float)p.guidance, (float)sig[t],
+        HIPCK(dit::launch_unipc(lat(j), vbuf, vpair ? vbuf + NC : nullptr, (float)p.guidance, (float)sig[t],
                                 l.x_last, (k.pp != 0.f || k.corr) ? m_s : nullptr, m_p, m_t, k, (int64_t)NC,
                                 c->stream));
       } else if (!folded) {
-        HIPCK(dit::launch_euler(lat(j), c->vel, pair ? c->vel + NC : nullptr, (float)p.guidance, dsig,
+        HIPCK(dit::launch_euler(lat(j), vbuf, pair ? vbuf + NC : nullptr, (float)p.guidance, dsig,
                                 (int64_t)NC, c->stream));
       }
       return DIT_OK;
@@ -1236,6 +1271,16 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
     for (int j = 0; j < S; ++j) {
       Lane& l = c->lanes[j];
       if (l.dec) continue;
+      if (step) {
+        // the candidate formed with the indicator is this step's result
+        if (!l.spec) return fail_all(t, DIT_EINVAL, "internal: reused step without a reuse candidate");
+        if (unipc) {
+          TRY(step_rule(j, false, false, l.vspec));
+        } else {
+          std::swap(cur[j], alt[j]);
+        }
+        continue;
+      }
       if (fused) {
         // h + r, final adaLN, projection, guidance and Euler in one pass per row tile
         Scope sc(c, DIT_K_REUSE, (double)nb * NH * c->esz);
@@ -1265,6 +1310,15 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
 
     // (a4) full: the computing samples' block stacks, (a5) per sample
     if (!comp.empty()) {
+      if (step)  // the block stack's input h, unless the indicator launch already wrote it
+        for (int j : comp) {
+          Lane& l = c->lanes[j];
+          if (!l.spec) continue;
+          Scope sc(c, DIT_K_FULL_OTHER, (double)NH * c->esz);
+          HIPCK(dit::launch_step_fused(lat(j), C, c->M.img_in.w, c->M.img_in.b, nullptr, nullptr, nullptr, N, H,
+                                       nullptr, nullptr, nullptr, nullptr, nullptr, nb, c->M.fin.w, c->M.fin.b,
+                                       nullptr, nullptr, 0.f, 0.f, nullptr, nullptr, l.h, c->stream));
+        }
       if (fused)  // the block stack's input h, bit-identical to the one the indicator used
         for (int j : comp) {
           Scope sc(c, DIT_K_FULL_OTHER, (double)NH * c->esz);
@@ -1313,6 +1367,9 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
       out[j].steps_done = t + 1;
     }
   }
+  for (int j = 0; j < S; ++j)
+    if (cur[j] != latents + j * NC)
+      HIPCK(hipMemcpyAsync(latents + j * NC, cur[j], NC * sizeof(float), hipMemcpyDeviceToDevice, c->stream));
   HIPCK(hipStreamSynchronize(c->stream));
   if (p.policy != DIT_POLICY_THRESHOLD)
     for (int j = 0; j < S; ++j)

@@ -112,6 +112,19 @@ hipError_t launch_reuse_indicator(const float* x, int C, const void* W_in, const
 hipError_t launch_reuse_final(float* x, int C, const void* W_in, const void* b_in, const void* r, int nb,
                               const void* W_out, const void* b_out, const float* mod0, const float* mod1,
                               float dsig, float guidance, int rows, int H, float* vout, hipStream_t s);
+// One step's streaming work fused (bf16, C = 64): the embedding once in LDS;
+// with m_out != nullptr m_t and (with m_prev != nullptr, partials !=
+// nullptr) the four relative-L1 sums into out[4]; with r != nullptr also the
+// reuse candidate of nb branches: x + dsig v into x_spec (x is not
+// modified), or v into v_spec when v_spec != nullptr; with h_out != nullptr
+// the embedding h itself.  mf_b = the branch's final (shift, scale), [2H] f32.
+bool step_fused_fits(int C, int H, int nb);
+int step_fused_partials(int rows, int H, int nb);
+hipError_t launch_step_fused(const float* x, int C, const void* W_in, const void* b_in, void* m_out,
+                             const void* m_prev, const void* m_last, int rows, int H, const float* sh0,
+                             const float* sc0, double* partials, double* out, const void* r, int nb,
+                             const void* W_out, const void* b_out, const float* mf0, const float* mf1, float dsig,
+                             float guidance, float* x_spec, float* v_spec, void* h_out, hipStream_t s);
 // y = S(LN(S(a + b))(1+sc)+sh) per row (reuse-step final-layer input).
 template <typename T>
 hipError_t launch_add_ln_mod(const T* a, const T* b, T* out, int rows, int H, const float* sh,
