@@ -29,17 +29,20 @@ def say(*a):
     print(*a, flush=True)
 
 
-def reduced_parity(name, T, B, **kw):
+def reduced_parity(name, T, B, n_img=None, **kw):
     torch = torch_cuda()
     w = synth.reduced(synth.workload(name), T=T, B=B, **kw)
+    if n_img is not None:
+        m = dataclasses.replace(w.model, n_img=n_img, name=w.model.name + f"_{n_img}")
+        w = dataclasses.replace(w, model=m, name=m.name)
     cfg = w.model
     t0 = time.time()
     weights, x0, text, gate = synth.make_inputs(w)
-    x_gpu, sched, h = run_sampler(torch, w, weights, x0, text, gate)
+    x_gpu, sched, h = run_sampler(torch, w, weights, x0, text, gate, solver=w.solver)
     h.close()
     say(f"{w.name}: device schedule {sched.full.tolist()} ({time.time() - t0:.1f} s)")
     ores = oracle_sample(cfg, weights.tensors, gate, x0, text, T, B, shift=w.shift,
-                         guidance=w.guidance, forced_mask=sched.full)
+                         guidance=w.guidance, forced_mask=sched.full, solver=w.solver)
     say(f"{w.name}: oracle done ({time.time() - t0:.1f} s)")
     check_schedule_against_oracle(sched, ores)
     check_logits(sched, ores, gate)
@@ -51,6 +54,24 @@ def reduced_parity(name, T, B, **kw):
 
 def test_flux1024_width_one_block_each():
     reduced_parity("flux1024", T=4, B=2, n_double=1, n_single=1)
+
+
+def test_flux1024_two_blocks_each():
+    """Two double and two single blocks: the hidden state crosses block
+    boundaries of both kinds and the double -> single hand-over."""
+    reduced_parity("flux1024", T=3, B=2, n_double=2, n_single=2)
+
+
+def test_flux2048_full_tokens_one_block_each():
+    """FLUX-2048 at its real token count (16384 image + 512 text tokens): one
+    computed and one reused step through one double and one single block."""
+    reduced_parity("flux2048", T=2, B=1, n_double=1, n_single=1)
+
+
+def test_wan_width_unipc_8192_tokens():
+    """The Wan block at H = 5120 with the workload's UniPC step rule (second
+    order at the middle step), 8192 video tokens."""
+    reduced_parity("wan14b", T=3, B=2, n_cross=1, n_img=8192)
 
 
 def test_qwen_guidance_pair_width_one_block():
@@ -144,27 +165,37 @@ def test_full_depth_properties(name):
 
 
 @pytest.mark.parametrize("L,heads,label", [(16384 + 512, 24, "flux2048"), (32760, 40, "wan14b")])
-def test_attention_long_sequences_sampled(L, heads, label):
+@pytest.mark.parametrize("bounded", [False, True])
+def test_attention_long_sequences_sampled(L, heads, label, bounded):
+    """Long-sequence attention on sampled query rows.  bounded: the sampler's
+    launch (q and k leave a unit-gain RMS norm, DIT_ATTN_BOUNDED_LOGITS, the
+    software-pipelined kernel); otherwise the running-maximum kernel."""
     torch = torch_cuda()
     rng = np.random.default_rng(7)
     H = heads * 128
     # bf16 values from torch's own rounding on the device would bypass the
     # oracle; draw on the host and round with the oracle's rule instead
-    def mk(n):
-        x = round_bf16(rng.standard_normal((n, H)).astype(np.float32).astype(np.float64))
+    def mk(n, norm):
+        x = rng.standard_normal((n, H)).astype(np.float32).astype(np.float64)
+        if norm:
+            x = dit.rms_heads(x * 3.0, heads, 128)
+        x = round_bf16(x)
         return (x.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16), x
-    q_b, q = mk(L)
-    k_b, k = mk(L)
-    v_b, v = mk(L)
+    q_b, q = mk(L, bounded)
+    k_b, k = mk(L, bounded)
+    v_b, v = mk(L, False)
     o = torch.zeros((L, H), dtype=torch.int16, device="cuda")
     ws = torch.zeros(heads * 128 * ((L + 63) // 64 * 64), dtype=torch.int16, device="cuda")
     binding.attention_bf16(dev(torch, q_b), dev(torch, k_b), dev(torch, v_b), o, Lq=L, Lk=L, heads=heads,
-                           ldq=H, ldk=H, ldv=H, ldo=H, vt_ws=ws)
+                           ldq=H, ldk=H, ldv=H, ldo=H, vt_ws=ws,
+                           flags=binding.ATTN_BOUNDED_LOGITS if bounded else 0)
     got = host_bf16(o)
-    rows = np.sort(rng.choice(L, 24, replace=False))
+    # the first and last query rows, a row of the ragged last tile and random rows
+    rows = np.unique(np.r_[0, L - 1, (L // 256) * 256 + 1 if L % 256 else L - 2,
+                           rng.choice(L, 24, replace=False)])
     ref = round_bf16(dit.attention(q[rows], k, v, heads, 128))
     err = rel_l2(got[rows], ref)
-    say(f"{label} attention L={L}: sampled rel-L2 {err:.2e}")
+    say(f"{label} attention L={L} bounded={bounded}: sampled rel-L2 {err:.2e}")
     assert err < 4e-3
 
 
