@@ -18,9 +18,7 @@
 // each iteration overlaps the softmax of one key tile (VALU) with the PV
 // product of the previous tile and the score product of the next (MFMA).
 #include <math.h>
-#include <stdlib.h>
 
-#include <string>
 
 #include "common.h"
 #include "kernels.h"
@@ -545,20 +543,12 @@ hipError_t launch_flash_attn_bf16(const void* q, int64_t ldq, const void* k, int
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
   const dim3 grid((Lq + QB - 1) / QB, heads, nseq);
   const SeqMap sm{split, gap, gz, zs};
-  // bounded logits take the software-pipelined kernel; DIT_ATTN_KERNEL=base
-  // selects the single-stage one (experiments)
-  static const bool pipe = [] {
-    const char* e = getenv("DIT_ATTN_KERNEL");
-    return !(e && std::string(e) == "base");
-  }();
-  if (bounded_logits && pipe)
+  // bounded logits take the software-pipelined kernel, the others the
+  // single-stage kernel with a running maximum
+  if (bounded_logits)
     hipLaunchKernelGGL((flash_attn_pipe_kernel<kNW>), dim3(grid.x * heads, 1, nseq), dim3(64 * kNW), 0, s,
                        (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o, ldo, Lq,
                        Lk, scale_log2, sm);
-  else if (bounded_logits)
-    hipLaunchKernelGGL((flash_attn_bf16_kernel<true, kQG, kNW>), grid, dim3(64 * kNW), 0, s,
-                       (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o,
-                       ldo, Lq, Lk, scale_log2, sm);
   else
     hipLaunchKernelGGL((flash_attn_bf16_kernel<false, kQG, kNW>), grid, dim3(64 * kNW), 0, s,
                        (const bf16_t*)q, ldq, (const bf16_t*)k, ldk, (const bf16_t*)vt, ldvt, (bf16_t*)o,

@@ -635,6 +635,7 @@ struct Seq {
   void* r;            // [N, H] refreshed residual (out)
   const float* mod;   // this step's modulation vector [n_mod]
   const float* modx;  // video blocks: base of [n_cross][T][6H]
+  const void* m0;     // [N, H] the first block's modulated image input (m_t), or nullptr
 };
 
 // One sequence at a time (f32 storage, video blocks).
@@ -651,8 +652,10 @@ dit_status full_stack(dit_cache* c, const Seq& q, int t, int T) {
     for (int i = 0; i < c->cfg.n_cross; ++i) {
       const CrossW& w = c->M.crs[i];
       const float* e = q.modx + ((size_t)i * T + t) * 6 * H;
-      TRY(ln_mod(c, c->X, H, c->A, H, N, N, e, e + H, e, e + H, DIT_K_FULL_OTHER));
-      GemmArgs g = lin_args(c, c->A, H, w.qkv, c->Y, ldY, N);
+      // block 0's modulated input is this step's indicator tensor m_t
+      const bool use_m0 = i == 0 && q.m0;
+      if (!use_m0) TRY(ln_mod(c, c->X, H, c->A, H, N, N, e, e + H, e, e + H, DIT_K_FULL_OTHER));
+      GemmArgs g = lin_args(c, use_m0 ? q.m0 : c->A, H, w.qkv, c->Y, ldY, N);
       g.rms_cols = 2 * H;
       TRY(gemm(c, &g, 1, cls));
       TRY(attention(c, c->Y, ldY, sp(c, c->Y, H), ldY, sp(c, c->Y, 2 * H), ldY, sp(c, c->Y, 3 * H), ldY, N,
@@ -698,9 +701,11 @@ dit_status full_stack(dit_cache* c, const Seq& q, int t, int T) {
     const DoubleW& w = c->M.dbl[i];
     const float* mi = md + (size_t)12 * H * i;  // image stream chunk
     const float* mt = mi + 6 * H;               // text stream chunk
-    TRY(ln_mod(c, c->X, H, c->A, H, L, Nt, mt, mt + H, mi, mi + H, DIT_K_FULL_OTHER));
+    // block 0's image-stream input is this step's indicator tensor m_t
+    const bool use_m0 = i == 0 && q.m0;
+    TRY(ln_mod(c, c->X, H, c->A, H, use_m0 ? Nt : L, Nt, mt, mt + H, mi, mi + H, DIT_K_FULL_OTHER));
     GemmArgs g[2];
-    g[0] = lin_args(c, Ai, H, w.qkv[0], Yi, ldY, N);
+    g[0] = lin_args(c, use_m0 ? q.m0 : (const void*)Ai, H, w.qkv[0], Yi, ldY, N);
     g[1] = lin_args(c, c->A, H, w.qkv[1], c->Y, ldY, Nt);
     g[0].rms_cols = g[1].rms_cols = 2 * H;
     TRY(gemm(c, g, 2, cls));
@@ -843,12 +848,17 @@ dit_status full_stack_multi(dit_cache* c, const Seq* seqs, int Q) {
     g.vt_rows0 = rows0; g.vt_key0 = key0;
     g.vt_rows1 = rows1; g.vt_key1 = key1;
   };
+  // one sequence: block 0's image-stream input is this step's indicator tensor m_t
+  const void* m0 = Q == 1 ? seqs[0].m0 : nullptr;
   for (int i = 0; i < c->cfg.n_double; ++i) {
     const DoubleW& w = c->M.dbl[i];
     const size_t mi = (size_t)12 * H * i, mt = mi + 6 * H;  // image / text stream chunks
-    TRY(lnm(mt, mi));
+    const bool use_m0 = i == 0 && m0;
+    if (use_m0) TRY(ln_mod(c, c->X, H, c->A, H, Lt, Lt, mr.base + mt, mr.base + mt + H, mr.base + mt,
+                           mr.base + mt + H, DIT_K_FULL_OTHER));
+    else TRY(lnm(mt, mi));
     GemmArgs g[2];
-    g[0] = lin_args(c, Ai, H, w.qkv[0], Yi, ldY, Li);
+    g[0] = lin_args(c, use_m0 ? m0 : (const void*)Ai, H, w.qkv[0], Yi, ldY, Li);
     g[1] = lin_args(c, c->A, H, w.qkv[1], c->Y, ldY, Lt);
     g[0].rms_cols = g[1].rms_cols = 2 * H;
     with_vt(g[0], N, Nt);   // image rows: keys Nt .. Nt + N - 1 of sequence m / N
@@ -1329,8 +1339,10 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
       for (int j : comp)
         for (int b = 0; b < nb; ++b) {
           Lane& l = c->lanes[j];
+          // the indicator tensor is the first block's modulated image input of branch 0
+          const void* m0 = (p.indicator == DIT_INDICATOR_MODULATED && b == 0) ? l.mbuf[l.i_new] : nullptr;
           seqs.push_back(Seq{sp(c, l.txt, (size_t)b * c->Nt * H), l.h, sp(c, l.r, b * NH), modp(j, b, t),
-                             modxp(j, b)});
+                             modxp(j, b), m0});
         }
       const int Q = (int)seqs.size();
       if (c->stacked) TRY(full_stack_multi(c, seqs.data(), Q));

@@ -952,14 +952,6 @@ Prob make_prob(const GemmArgs& g, int bm, int bn) {
   return p;
 }
 
-int forced_cfg() {
-  static int v = [] {
-    const char* e = getenv("DIT_GEMM_CONFIG");
-    return e ? atoi(e) : -1;
-  }();
-  return v;
-}
-
 int pick_cfg(const GemmArgs* g, int n, int n_cu) {
   bool rms = false, aligned = true;
   for (int i = 0; i < n; ++i) {
@@ -987,8 +979,6 @@ int pick_cfg(const GemmArgs* g, int n, int n_cu) {
       if (g[i].K % k.bk || g[i].K < k.min_k) return false;
     return true;
   };
-  const int f = forced_cfg();
-  if (f >= 0 && f < kNumCfgs && admits(kCfgs[f])) return f;
   bool shallow = true;  // K <= 256: the tile writes dominate, more workgroups stream better
   for (int i = 0; i < n; ++i) shallow &= g[i].K <= 256 && g[i].M >= 512;
   if (shallow)
