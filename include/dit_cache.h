@@ -200,6 +200,15 @@ dit_status dit_cache_sample_batch(dit_cache* h, int32_t n_samples, float* latent
                                   const float* gate_weights, size_t gate_len,
                                   const dit_sample_params* p, dit_schedule* out);
 
+/* The gate of Eq. 1 alone, on the host in double precision: *logit =
+ * z = g_theta(f) for one 8-feature state f (features[0..7], the layout of
+ * dit_schedule.features; a gate with d_0 < 8 inputs reads f_0..f_{d_0-1}),
+ * from the same self-describing blob dit_cache_sample takes (plain MLP or
+ * the branched form of App. A.2, optional z-scoring).  Alg. 2 computes when
+ * z > ln(tau / (1 - tau)).  Needs no device.  Errors: DIT_EINVAL (null
+ * pointer or malformed blob; the message via dit_cache_last_error(NULL)). */
+dit_status dit_gate_logit(const float* gate_weights, size_t gate_len, const double* features, double* logit);
+
 void dit_cache_destroy(dit_cache* h);
 
 /* Last error message of this handle ("" if none).  With h == NULL: the last

@@ -30,7 +30,7 @@ K_CLASSES = ["gemm", "attn", "indicator", "reuse", "full_other", "once"]
 
 # Every symbol the headers declare.
 EXPORTS = ["dit_cache_create", "dit_cache_sample", "dit_cache_sample_ex", "dit_cache_sample_batch",
-           "dit_cache_destroy",
+           "dit_gate_logit", "dit_cache_destroy",
            "dit_cache_last_error", "dit_cache_set_profiling", "dit_cache_get_stats",
            "dit_cache_reset_stats", "dit_gemm_bf16", "dit_attention_bf16", "dit_attention_bf16_noalloc"]
 
@@ -92,6 +92,7 @@ def load(path: str = LIB_PATH):
     lib.dit_cache_sample_ex.argtypes = [vp, vp, vp, vp, sz, C.POINTER(SampleParamsC), C.POINTER(ScheduleC)]
     lib.dit_cache_sample_batch.argtypes = [vp, C.c_int32, vp, vp, vp, sz, C.POINTER(SampleParamsC),
                                            C.POINTER(ScheduleC)]
+    lib.dit_gate_logit.argtypes = [vp, sz, vp, vp]
     lib.dit_cache_destroy.argtypes = [vp]
     lib.dit_cache_destroy.restype = None
     lib.dit_cache_last_error.argtypes = [vp]
@@ -298,3 +299,17 @@ def attention_bf16_noalloc(q, k, v, o, *, Lq, Lk, heads, ldq, ldk, ldv, ldo, fla
     st = lib.dit_attention_bf16_noalloc(q.data_ptr(), ldq, k.data_ptr(), ldk, v.data_ptr(), ldv,
                                         o.data_ptr(), ldo, Lq, Lk, heads, flags, _stream_ptr(stream))
     _check(st, None)
+
+
+def gate_logit(gate_blob, features) -> float:
+    """dit_gate_logit: the library's host gate on one 8-feature state."""
+    lib = load()
+    gate = np.ascontiguousarray(gate_blob, np.float32)
+    f = np.ascontiguousarray(np.asarray(features, np.float64).reshape(-1)[:N_FEATURES])
+    if f.size < N_FEATURES:
+        f = np.concatenate([f, np.zeros(N_FEATURES - f.size)])
+    out = C.c_double()
+    st = lib.dit_gate_logit(gate.ctypes.data_as(C.c_void_p) if gate.size else None, gate.size,
+                            f.ctypes.data_as(C.c_void_p), C.byref(out))
+    _check(st, None)
+    return out.value

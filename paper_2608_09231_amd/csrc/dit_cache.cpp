@@ -1504,6 +1504,15 @@ dit_status dit_cache_sample(dit_cache* c, float* latent, const void* text_emb, i
   return dit_cache_sample_ex(c, latent, text_emb, gate_weights, gate_len, &p, out);
 }
 
+dit_status dit_gate_logit(const float* gate_weights, size_t gate_len, const double* features, double* logit) {
+  g_create_error.clear();
+  if (!features || !logit) return fail(nullptr, DIT_EINVAL, "null argument");
+  GateMLP g;
+  TRY(parse_gate(nullptr, gate_weights, gate_len, g));
+  *logit = gate_logit(g, features);
+  return DIT_OK;
+}
+
 void dit_cache_destroy(dit_cache* c) {
   if (!c) return;
   if (c->stream) hipStreamSynchronize(c->stream);

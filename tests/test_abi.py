@@ -89,3 +89,124 @@ def test_noalloc_attention_rejects_oversized_on_the_host():
     assert "allocation-free limit" in lib.dit_cache_last_error(None).decode()
     st = lib.dit_attention_bf16_noalloc(None, H, fake, H, fake, H, fake, H, 8, 8, 24, 0, None)
     assert st == binding.DIT_EINVAL
+
+
+# ---------------------------------------------------------------- host gate
+
+def _gates():
+    from tests.test_gpu_sampler import FLIP, flip_gate
+    mu = np.array([0.4, 0.5, 0.6, 2.0, 0.1, 0.05], np.float32)
+    sd = np.array([0.2, 0.3, 0.4, 1.5, 0.1, 0.05], np.float32)
+    gates = [synth.make_gate_blob((8, 32, 16, 1), seed=0),
+             synth.make_gate_blob((8, 32, 16, 1), seed=3, std=1.0),
+             synth.make_gate_blob((6, 8, 8, 32, 1), seed=11, zscore=(mu, sd)),
+             synth.make_branched_gate_blob(seed=5, zscore=(mu, sd)),
+             synth.make_branched_gate_blob(seed=2)]
+    gates += [flip_gate(c) for c in FLIP["cases"].values()]
+    return gates
+
+
+def test_host_gate_matches_the_oracle_gate():
+    """dit_gate_logit (the gate the sampler evaluates between launches) is
+    Eq. 1's network as the oracle reads it, for the plain, z-scored and
+    branched blobs, on random states around the workloads' feature ranges."""
+    from oracle import parse_gate_blob
+    rng = np.random.default_rng(9)
+    for blob in _gates():
+        g = parse_gate_blob(blob)
+        for _ in range(40):
+            f = np.r_[rng.uniform(0, 1, 3), rng.integers(1, 12), rng.uniform(0, 0.5, 2), rng.uniform(0, 1),
+                      rng.uniform(0, 2)]
+            z = binding.gate_logit(blob, f)
+            ref = g.logit(f)
+            assert abs(z - ref) <= 1e-12 * (1 + abs(ref)), (z, ref)
+
+
+def test_host_gate_rejects_malformed_blobs():
+    good = synth.make_gate_blob((8, 32, 16, 1), seed=0)
+    bad = [good[:-1], np.r_[good, 0.0], good[:3]]
+    b = good.copy(); b[0] = 1.5; bad.append(b)                 # fractional layer count
+    b = good.copy(); b[4] = 2; bad.append(b)                   # output width != 1
+    b = good.copy(); b[1] = 9; bad.append(b)                   # more than 8 inputs
+    br = synth.make_branched_gate_blob(seed=5)
+    b = br.copy(); b[10] = 15; bad.append(b)                   # trunk input != branch outputs
+    b = br.copy(); b[0] = -20; bad.append(b)                   # branch count
+    f = np.zeros(8)
+    for blob in bad:
+        with pytest.raises(binding.DitError) as e:
+            binding.gate_logit(blob, f)
+        assert e.value.status == binding.DIT_EINVAL
+    with pytest.raises(binding.DitError):
+        binding.gate_logit(np.zeros(0, np.float32), f)
+
+
+# ------------------------------------------------- sanitized host driver
+
+_SAN_SCRIPT = r"""
+import ctypes as C, sys
+import numpy as np
+sys.path.insert(0, sys.argv[2])
+from paper_2608_09231_amd import binding, synth
+lib = binding.load(sys.argv[1])
+rng = np.random.default_rng(0)
+# gate parsing on valid, truncated and randomly corrupted blobs
+blobs = [synth.make_gate_blob((8, 32, 16, 1), seed=0), synth.make_gate_blob((6, 8, 8, 32, 1), seed=1),
+         synth.make_branched_gate_blob(seed=5)]
+f = np.linspace(0.1, 0.8, 8)
+out = C.c_double()
+n_ok = 0
+for base in blobs:
+    for trial in range(400):
+        b = base.copy()
+        if trial % 4 == 1:
+            b = b[: rng.integers(0, b.size)]
+        elif trial % 4 == 2:
+            i = rng.integers(0, min(b.size, 16))
+            b[i] = rng.choice([-3.0, -1.0, 0.0, 1.0, 2.5, 7.0, 9.0, 1e9, -1e9, np.nan, np.inf])
+        elif trial % 4 == 3:
+            b = np.r_[b, rng.standard_normal(rng.integers(1, 5)).astype(np.float32)]
+        b = np.ascontiguousarray(b, np.float32)
+        st = lib.dit_gate_logit(b.ctypes.data_as(C.c_void_p) if b.size else None, b.size,
+                                f.ctypes.data_as(C.c_void_p), C.byref(out))
+        assert st in (0, -1), st
+        n_ok += st == 0
+        lib.dit_cache_last_error(None)
+# configuration checks of create (no device memory is touched before they pass)
+wl = synth.workload("tiny")
+for field, val in (("abi_version", 99), ("heads", 3), ("hidden", -1), ("batch", 3), ("n_cross", 2),
+                   ("dtype", 7), ("head_dim", 0), ("n_img", 0)):
+    cfg = binding.model_config_c(wl.model)
+    setattr(cfg, field, val)
+    h = C.c_void_p()
+    blob = np.zeros(4, np.float32)
+    st = lib.dit_cache_create(C.byref(cfg), blob.ctypes.data_as(C.c_void_p), blob.nbytes, None, C.byref(h))
+    assert st < 0, (field, st)
+    assert len(lib.dit_cache_last_error(None)) > 0
+fake = C.c_void_p(0x1000)
+assert lib.dit_attention_bf16_noalloc(fake, 3072, fake, 3072, fake, 3072, fake, 3072, 8, 5441, 24, 0, None) < 0
+print("SANITIZED-OK", n_ok)
+"""
+
+
+def test_host_driver_under_address_and_ub_sanitizers(tmp_path):
+    """The host driver built with AddressSanitizer and UBSan (host code
+    only) runs the device-free entry points -- gate parsing on valid,
+    truncated and corrupted blobs, create's configuration checks, the
+    allocation-free attention's size check -- without a sanitizer report."""
+    import subprocess
+    import sys
+
+    from paper_2608_09231_amd import build
+    lib = build.build_sanitized()
+    rt = build.sanitizer_runtime()
+    if not os.path.exists(rt):
+        pytest.skip("no AddressSanitizer runtime")
+    script = tmp_path / "san.py"
+    script.write_text(_SAN_SCRIPT)
+    env = dict(os.environ, LD_PRELOAD=rt, ASAN_OPTIONS="detect_leaks=0:abort_on_error=0",
+               UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1")
+    r = subprocess.run([sys.executable, str(script), lib, ROOT], capture_output=True, text=True, env=env,
+                       timeout=300)
+    assert r.returncode == 0, r.stderr[-4000:]
+    assert "SANITIZED-OK" in r.stdout
+    assert "AddressSanitizer" not in r.stderr and "runtime error" not in r.stderr, r.stderr[-4000:]
