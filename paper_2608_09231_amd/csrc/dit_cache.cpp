@@ -657,9 +657,21 @@ dit_status full_stack(dit_cache* c, const Seq& q, int t, int T) {
       if (!use_m0) TRY(ln_mod(c, c->X, H, c->A, H, N, N, e, e + H, e, e + H, DIT_K_FULL_OTHER));
       GemmArgs g = lin_args(c, use_m0 ? q.m0 : c->A, H, w.qkv, c->Y, ldY, N);
       g.rms_cols = 2 * H;
+      // the projection writes the values transposed for attention when it can
+      bool vt_fused = false;
+      if (c->bf16) {
+        g.vt = c->vt;
+        g.vt_col0 = 2 * H;
+        g.vt_heads = c->cfg.heads;
+        g.vt_ld = (int)rup(N, 64);
+        g.vt_rows0 = N;
+        g.vt_key0 = 0;
+        vt_fused = dit::gemm_bf16_fuses_vt(&g, 1, c->n_cu);
+        if (!vt_fused) g.vt = nullptr;
+      }
       TRY(gemm(c, &g, 1, cls));
       TRY(attention(c, c->Y, ldY, sp(c, c->Y, H), ldY, sp(c, c->Y, 2 * H), ldY, sp(c, c->Y, 3 * H), ldY, N,
-                    N, c->vt));
+                    N, c->vt, 0x7fffffff, 0, 1, 0, 0, vt_fused));
       g = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.o, c->X, H, N, DIT_EPI_GATED_RES);
       g.gate = e + 2 * H;
       TRY(gemm(c, &g, 1, cls));

@@ -644,7 +644,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_dma_kernel(Batch b) 
 // slots 8 lhalf .. 8 lhalf + 7 of the first group and r = 8..15 the same
 // slots of the second, so each lane stores two 16-byte runs per block.  The
 // host admits this only for 32-row aligned segments (a block is one
-// sequence's keys kb .. kb + 31, kb a multiple of 32).
+// sequence's keys kb .. kb + 31, kb a multiple of 32), or for one sequence in
+// one piece, whose last block may end past its last key inside the padded
+// key range).
 __device__ __forceinline__ void store_vt(const Prob& P, const f32x16_t (&acc)[2][4], int m_base, int ncol0,
                                          int lrow, int lhalf) {
   const int h = (ncol0 - P.vt_col0) >> 7;
@@ -1051,7 +1053,15 @@ static bool vt_ok(const GemmArgs* g, int n, int c) {
     const int end = a.vt_col0 + 128 * a.vt_heads;
     if (a.vt_heads < 1 || a.vt_col0 % 128 || end > a.N || a.vt_ld % 8 || ((uintptr_t)a.vt & 15)) return false;
     if (a.vt_col0 < a.rms_cols || end > a.gelu_from || (a.gap && end > a.gap_at)) return false;
-    if (a.M % 32 || a.vt_rows0 % 32 || a.vt_key0 % 32 || a.vt_rows0 < 1) return false;
+    // one sequence in one piece may end inside a 32-row block: that block's
+    // rows past M repeat row M - 1 (clamped loads), so the keys it writes past
+    // the sequence hold finite values that attention masks out
+    const bool single = a.vt_split >= a.M && a.vt_rows0 >= a.M;
+    if (single) {
+      if (a.vt_key0 % 32 || a.vt_key0 + (a.M + 31) / 32 * 32 > a.vt_ld) return false;
+    } else if (a.M % 32 || a.vt_rows0 % 32 || a.vt_key0 % 32 || a.vt_rows0 < 1) {
+      return false;
+    }
     if (a.vt_split < a.M && (a.vt_split % 32 || a.vt_rows1 % 32 || a.vt_key1 % 32 || a.vt_rows1 < 1)) return false;
   }
   return true;
