@@ -1176,7 +1176,9 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
         else if (p.policy == DIT_POLICY_STATIC) known_full = known_full || mu[t];
         l.spec = !known_full;
         const int reads = t == 0 ? 0 : (l.i_prev == l.i_last ? 1 : 2);
-        Scope sc(c, DIT_K_INDICATOR, (double)NH * c->esz * (1 + reads + (l.spec ? nb : 0)));
+        // algorithmic bytes: m_t written, m_{t-1} / m_last read, and either r read per branch
+        // (reuse candidate) or h written (the block stack's input)
+        Scope sc(c, DIT_K_INDICATOR, (double)NH * c->esz * (1 + reads + (l.spec ? nb : 1)));
         const float* mf0 = modp(j, 0, t) + (c->n_mod - 2 * H);
         const float* mf1 = pair ? modp(j, 1, t) + (c->n_mod - 2 * H) : nullptr;
         HIPCK(dit::launch_step_fused(lat(j), C, c->M.img_in.w, c->M.img_in.b, l.mbuf[l.i_new], mp, ml, N, H, sh0, sc0,
