@@ -185,8 +185,9 @@ def multi_prompt(h, w, lat0, args, ms_single):
     torch.cuda.synchronize()
     h.reset_stats()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
         scheds = one()
+        log(f"[bench] multi-prompt batch {i + 1}/{args.steps} done at {time.perf_counter() - t0:.1f} s")
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     st = h.stats()
@@ -271,6 +272,8 @@ def main():
     t0 = time.perf_counter()
     for i in range(args.steps):
         s = one()
+        # one line per sample (a host print after the sample has drained)
+        log(f"[bench] timed sample {i + 1}/{args.steps} done at {time.perf_counter() - t0:.1f} s")
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     st = h.stats()
