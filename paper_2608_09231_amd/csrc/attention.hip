@@ -19,6 +19,8 @@
 // product of the previous tile and the score product of the next (MFMA).
 #include <math.h>
 
+#include <type_traits>
+
 
 #include "common.h"
 #include "kernels.h"
@@ -265,7 +267,13 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_bf16_kernel(
 // Software-pipelined variant (bounded logits only): iteration t runs the
 // PV product of tile t-1 and the score product of tile t+1 (MFMA) together
 // with the softmax of tile t (VALU), which depends on neither.  Five LDS
-// stages: tiles t-1 (V), t, t+1 (K), t+2 and t+3 (in flight).
+// stages: tiles t-1 (V), t, t+1 (K), t+2 and t+3 (in flight).  The loop is
+// unrolled by two so the score and probability buffers alternate statically
+// (no register copies), each lane's fragment offsets inside a stage are
+// computed once (one add of the stage base per offset and tile), and in the
+// steady state a tile's copies take one uniform base plus fixed per-lane
+// byte offsets.  Each steady iteration is scheduled explicitly: three LDS
+// reads ahead, then per MFMA one read and four VALU instructions.
 constexpr int PSTAGE = 5;
 
 // Work-groups are dispatched to the 8 XCDs round-robin (block b to XCD
@@ -276,12 +284,25 @@ __device__ __forceinline__ int xcd_order(int b, int n) {
   return x * q + (x < r ? x : r) + (b >> 3);
 }
 
+// Instruction-group order for the scheduler over one loop iteration: RA LDS
+// reads first, then per MFMA one read (while reads remain) and VG VALU ops.
+template <int RA, int VG, int NM, int ND>
+__device__ __forceinline__ void sched_pattern() {
+  __builtin_amdgcn_sched_group_barrier(0x100, RA, 0);  // DS read
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    if (i < ND - RA) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, VG, 0);  // VALU
+  }
+}
+
 template <int NW>
 __global__ __launch_bounds__(64 * NW) void flash_attn_pipe_kernel(
     const bf16_t* __restrict__ q, int64_t ldq, const bf16_t* __restrict__ k, int64_t ldk,
     const bf16_t* __restrict__ vt, int ldvt, bf16_t* __restrict__ o, int64_t ldo, int Lq, int Lk,
     float scale_log2, SeqMap sm) {
-  __shared__ __attribute__((aligned(1024))) char smem[PSTAGE][TILE_BYTES];  // [stage][K | V^T]
+  __shared__ __attribute__((aligned(1024))) char smem[PSTAGE * TILE_BYTES];  // [stage][K | V^T]
   const RowMap rm = sm.at(blockIdx.z);
 
   constexpr int QB = NW * 32;
@@ -306,9 +327,11 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_pipe_kernel(
   }
   const bf16_t* kh = k + h * D;
   const bf16_t* vh = vt + (int64_t)h * D * ldvt;
-  auto issue_tile = [&](int t) {
+  // copies of tile t into the stage at byte offset so: K rows 4 ii .. 4 ii + 3
+  // and V^T rows 8 ii .. 8 ii + 7 for ii = CPW wave + j (any tile)
+  auto issue_tile = [&](int t, int so) {
     const int kb0 = t * KT;
-    char* sk = smem[t % PSTAGE];
+    char* sk = smem + so;
     char* sv = sk + KT * D * 2;
 #pragma unroll
     for (int j = 0; j < CPW; ++j) {
@@ -328,8 +351,41 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_pipe_kernel(
       }
     }
   };
-  auto scores = [&](int t, f32x16_t (&sacc)[2]) {
-    const char* sk = smem[t % PSTAGE];
+  // the same copies for a full tile on one side of the split: a uniform base
+  // per tile plus this lane's fixed byte offsets (32-bit: ldk, ldvt < 2^24)
+  const bool narrow = ldk < (1 << 24) && ldvt < (1 << 24);
+  const int ldk32 = narrow ? (int)ldk : 0, ldvt32 = narrow ? ldvt : 0;
+  uint32_t kvo[CPW], vvo[CPW];
+#pragma unroll
+  for (int j = 0; j < CPW; ++j) {
+    const int ii = wave * CPW + j;
+    const int row = 4 * ii + (lane >> 4);
+    kvo[j] = (uint32_t)(row * ldk32 + (((lane & 15) ^ (row & 15)) << 3)) * 2u;
+    const int d = 8 * ii + (lane >> 3);
+    vvo[j] = (uint32_t)(d * ldvt32 + (((lane & 7) ^ ((d >> 1) & 7)) << 3)) * 2u;
+  }
+  auto issue_full = [&](int t, int so) {
+    const int kb0 = t * KT;
+    const char* kt0 = (const char*)(kh + rm(kb0) * ldk);
+    const char* vt0 = (const char*)(vh + kb0);
+    char* sk = smem + so;
+    char* sv = sk + KT * D * 2;
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) {
+      const int ii = wave * CPW + j;
+      __builtin_amdgcn_global_load_lds((glb_void_t*)(kt0 + kvo[j]), (lds_void_t*)(sk + ii * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((glb_void_t*)(vt0 + vvo[j]), (lds_void_t*)(sv + ii * 1024), 16, 0, 0);
+    }
+  };
+  // this lane's fragment offsets inside a stage: K per s (kb = 1 adds 8 KB),
+  // V^T per ks (dt adds 4 KB each)
+  int koff[8], voff[4];
+#pragma unroll
+  for (int s = 0; s < 8; ++s) koff[s] = k_off(lrow, 2 * s + lhalf);
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) voff[ks] = KT * D * 2 + v_off(lrow, 2 * ks + lhalf);
+  auto scores = [&](int so, f32x16_t (&sacc)[2]) {
+    const char* sk = smem + so;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -338,7 +394,7 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_pipe_kernel(
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
-        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sk + k_off(kb * 32 + lrow, 2 * s + lhalf)));
+        const bf16x8_t kf = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sk + koff[s] + kb * 32 * 256));
         sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
       }
   };
@@ -377,58 +433,76 @@ __global__ __launch_bounds__(64 * NW) void flash_attn_pipe_kernel(
     }
     l_run += ls;
   };
-  auto pv = [&](int t, const bf16x8_t (&pf)[4]) {
-    const char* sv = smem[t % PSTAGE] + KT * D * 2;
+  auto pv = [&](int so, const bf16x8_t (&pf)[4]) {
+    const char* sv = smem + so;
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sv + v_off(dt * 32 + lrow, 2 * ks + lhalf)));
+        const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sv + voff[ks] + dt * 32 * 128));
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], oacc[dt], 0, 0, 0);
       }
   };
   const int ntiles = (Lk + KT - 1) / KT;
-  f32x16_t s_cur[2], s_nxt[2];
-  bf16x8_t p_prv[4], p_cur[4];
-  // generic iteration (prologue and tail): every part guarded
-  auto iter_any = [&](int t) {
-    if (t + 3 < ntiles) issue_tile(t + 3);
-    if (t > 0) pv(t - 1, p_prv);
-    if (t + 1 < ntiles) scores(t + 1, s_nxt);
-    softmax(t, s_cur, p_cur, t * KT + KT > Lk);
-    // tile t+2 must have landed for the next iteration's scores; tile t+3 may stay in flight
+  // steady copies need every full tile on one side of the split and 32-bit
+  // lane offsets
+  const bool fast = (rm.split >= Lk || rm.split % KT == 0) && narrow;
+  f32x16_t sb[2][2];
+  bf16x8_t pb[2][4];
+  // stage byte offsets of tiles t - 1 (PV), t + 1 (scores) and t + 3 (copies)
+  // at iteration t, advanced once per iteration
+  constexpr int RING = PSTAGE * TILE_BYTES;
+  int so_pv = (PSTAGE - 1) * TILE_BYTES, so_sc = TILE_BYTES, so_is = 3 * TILE_BYTES;
+  auto advance = [&]() {
+    so_pv = so_pv + TILE_BYTES == RING ? 0 : so_pv + TILE_BYTES;
+    so_sc = so_sc + TILE_BYTES == RING ? 0 : so_sc + TILE_BYTES;
+    so_is = so_is + TILE_BYTES == RING ? 0 : so_is + TILE_BYTES;
+  };
+  // iteration t, buffers by the parity P of t: copies of tile t + 3; PV of
+  // tile t - 1; scores of t + 1; softmax of t; then tile t + 2 has landed
+  // (tile t + 3 may stay in flight) and every wave is done with tile t - 1
+  auto iter_any = [&](auto par_, int t) {
+    constexpr int P = decltype(par_)::value;
+    if (t + 3 < ntiles) issue_tile(t + 3, so_is);
+    if (t > 0) pv(so_pv, pb[P ^ 1]);
+    if (t + 1 < ntiles) scores(so_sc, sb[P ^ 1]);
+    softmax(t, sb[P], pb[P], t * KT + KT > Lk);
     if (t + 3 < ntiles) __builtin_amdgcn_s_waitcnt((2 * CPW) | (7 << 4) | (0 << 8));
     else __builtin_amdgcn_s_waitcnt(0);
     asm volatile("s_barrier" ::: "memory");
-#pragma unroll
-    for (int i = 0; i < 4; ++i) p_prv[i] = p_cur[i];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) s_cur[kb] = s_nxt[kb];
+    advance();
   };
-  // steady iteration: 0 < t, t + 3 < ntiles, tile t full
-  auto iter_steady = [&](int t) {
-    issue_tile(t + 3);
-    pv(t - 1, p_prv);
-    scores(t + 1, s_nxt);
-    softmax(t, s_cur, p_cur, false);
+  // 1 <= t, t + 4 < ntiles - 1: tiles t and t + 3 full, no guard
+  auto iter_steady = [&](auto par_, int t) {
+    constexpr int P = decltype(par_)::value;
+    issue_full(t + 3, so_is);
+    pv(so_pv, pb[P ^ 1]);
+    scores(so_sc, sb[P ^ 1]);
+    softmax(t, sb[P], pb[P], false);
+    sched_pattern<3, 4, 32, 32>();
     __builtin_amdgcn_s_waitcnt((2 * CPW) | (7 << 4) | (0 << 8));
     asm volatile("s_barrier" ::: "memory");
-#pragma unroll
-    for (int i = 0; i < 4; ++i) p_prv[i] = p_cur[i];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) s_cur[kb] = s_nxt[kb];
+    advance();
   };
-  for (int u = 0; u < 3 && u < ntiles; ++u) issue_tile(u);
+  for (int u = 0; u < 3 && u < ntiles; ++u) issue_tile(u, u * TILE_BYTES);
   // tiles 0 and 1 have landed (tile 2 may stay in flight)
   if (ntiles >= 3) __builtin_amdgcn_s_waitcnt((2 * CPW) | (7 << 4) | (0 << 8));
   else __builtin_amdgcn_s_waitcnt(0);
   asm volatile("s_barrier" ::: "memory");
-  scores(0, s_cur);
-  iter_any(0);
+  scores(0, sb[0]);
+  iter_any(std::integral_constant<int, 0>{}, 0);
   int t = 1;
-  for (; t + 3 < ntiles; ++t) iter_steady(t);
-  for (; t < ntiles; ++t) iter_any(t);
-  pv(ntiles - 1, p_prv);
+  for (; fast && t + 5 < ntiles; t += 2) {
+    iter_steady(std::integral_constant<int, 1>{}, t);
+    iter_steady(std::integral_constant<int, 0>{}, t + 1);
+  }
+  for (; t < ntiles; t += 2) {
+    iter_any(std::integral_constant<int, 1>{}, t);
+    if (t + 1 < ntiles) iter_any(std::integral_constant<int, 0>{}, t + 1);
+  }
+  // so_pv now holds tile ntiles - 1
+  if ((ntiles - 1) & 1) pv(so_pv, pb[1]);
+  else pv(so_pv, pb[0]);
 
   {
     const int qi = q0 + lrow;
