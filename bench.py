@@ -38,7 +38,7 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(w, rows=1024, q_sample=128):
+def cpu_baseline(w, rows=2048, q_sample=256):
     """Time the CPU oracle (as it stands) on a bounded sample of the same
     workload and extrapolate to one whole sample.
 
