@@ -23,7 +23,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = os.environ.get("DIT_OFFLOAD_ARCH", "gfx950")
 
 SOURCES = ["dit_cache.cpp", "gemm_bf16.hip", "gemm_f32.hip", "attention.hip", "stream_kernels.hip",
-           "reuse_kernels.hip"]
+           "reuse_kernels.hip", "step_stream.hip"]
 
 COMMON = [
     f"--offload-arch={ARCH}", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", "-Wno-unused-value", "-Wno-unused-result",

@@ -80,6 +80,7 @@ struct Lane {
   float* mh[3] = {};        // f32 [N, C]: UniPC data predictions (rotating)
   float* xalt = nullptr;    // f32 [N, C]: second latent buffer (the reuse candidate's Euler result)
   float* vspec = nullptr;   // f32 [N, C]: the reuse candidate's velocity (UniPC)
+  double* mag = nullptr;    // f64 [3]: sum |m| of each indicator buffer (column-sliced step kernel)
   int cnt = 0, t_last = 0, i_prev = -1, i_last = -1, i_new = 0;
   double acc = 0.0;
   bool dec = true;
@@ -119,6 +120,12 @@ struct dit_cache {
   float* ones = nullptr;   // f32 [H] (ungated residual)
   double* partials = nullptr;
   int max_partials = 0;
+  // column-sliced step kernel (bf16, C = 64): LN statistics matrix of the
+  // patch embedding (bf16 hi / lo [80][64]) and the candidate partials
+  void* st_hi = nullptr;
+  void* st_lo = nullptr;
+  float st_bbar = 0.f, st_b2 = 0.f;
+  float* cand = nullptr;
   double* sums_host = nullptr;  // pinned, mapped [lanes, 4]
   double* sums_dev = nullptr;
   int cap_sums = 0;
@@ -128,6 +135,7 @@ struct dit_cache {
   // one per branch of each sample with pooled text, else one)
   int cap_T = 0, cap_slots = 0;
   float* mod = nullptr;    // f32 [slots, T, n_mod]
+  float* fconst = nullptr; // f32 [slots, T, 128]: final-layer constants A | B of each table row
   float* modx = nullptr;   // f32 [slots, n_cross, T, 6H]
   void* temb = nullptr;    // [T, time_dim]
   void* th = nullptr;      // [T, H]
@@ -392,9 +400,22 @@ dit_status dalloc(dit_cache* c, P** p, size_t bytes) {
   return DIT_OK;
 }
 
+// LN statistics matrix of the patch embedding for the column-sliced step
+// kernel, from the host weight blob (W_in, b_in still blob offsets).
+dit_status upload_stream_stats(dit_cache* c, const uint16_t* blob) {
+  std::vector<uint16_t> hi((size_t)80 * 64), lo((size_t)80 * 64);
+  dit::step_stream_stats(blob + (uintptr_t)c->M.img_in.w, blob + (uintptr_t)c->M.img_in.b, c->H, hi.data(),
+                         lo.data(), &c->st_bbar, &c->st_b2);
+  TRY(dalloc(c, &c->st_hi, hi.size() * 2));
+  TRY(dalloc(c, &c->st_lo, lo.size() * 2));
+  HIPCK(hipMemcpy(c->st_hi, hi.data(), hi.size() * 2, hipMemcpyHostToDevice));
+  HIPCK(hipMemcpy(c->st_lo, lo.data(), lo.size() * 2, hipMemcpyHostToDevice));
+  return DIT_OK;
+}
+
 void free_lane(Lane& l) {
   void* ps[] = {l.h, l.mbuf[0], l.mbuf[1], l.mbuf[2], l.r, l.txt, l.x_last, l.mh[0], l.mh[1], l.mh[2],
-                l.xalt, l.vspec};
+                l.xalt, l.vspec, l.mag};
   for (void* p : ps)
     if (p) hipFree(p);
   l = Lane{};
@@ -411,6 +432,7 @@ dit_status alloc_lane(dit_cache* c, Lane& l) {
   for (auto& m : l.mh) TRY(dalloc(c, &m, NC * 4));
   TRY(dalloc(c, &l.xalt, NC * 4));
   TRY(dalloc(c, &l.vspec, NC * 4));
+  TRY(dalloc(c, &l.mag, 3 * sizeof(double)));
   return DIT_OK;
 }
 
@@ -479,17 +501,19 @@ dit_status alloc_workspace(dit_cache* c) {
     HIPCK(hipMemcpy(c->ones, one.data(), H * 4, hipMemcpyHostToDevice));
   }
   c->max_partials = std::max({dit::indicator_partials(N), dit::reuse_indicator_partials(N),
-                              dit::step_fused_partials(N, H, c->nb)});
+                              dit::step_fused_partials(N, H, c->nb), dit::step_stream_partials(N, H)});
+  if (c->bf16 && dit::step_stream_fits(c->C, H, c->nb))
+    TRY(dalloc(c, &c->cand, dit::step_stream_cand_floats(N, H, c->nb) * 4));
   TRY(dalloc(c, &c->partials, (size_t)c->max_partials * 4 * sizeof(double)));
   HIPCK(hipEventCreateWithFlags(&c->ev_sums, hipEventDisableTiming));
   return ensure_lanes(c, 1);
 }
 
 void free_per_call(dit_cache* c) {
-  void* ps[] = {c->mod, c->modx, c->temb, c->th, c->tv, c->pooled, c->ph, c->pv, c->svec, c->sig_dev};
+  void* ps[] = {c->mod, c->modx, c->temb, c->th, c->tv, c->pooled, c->ph, c->pv, c->svec, c->sig_dev, c->fconst};
   for (void* p : ps)
     if (p) hipFree(p);
-  c->mod = c->modx = c->tv = c->pv = nullptr;
+  c->mod = c->modx = c->tv = c->pv = c->fconst = nullptr;
   c->temb = c->th = c->pooled = c->ph = c->svec = nullptr;
   c->sig_dev = nullptr;
   c->cap_T = c->cap_slots = 0;
@@ -505,6 +529,7 @@ dit_status ensure_T(dit_cache* c, int T, int S) {
   const size_t e = c->esz;
   const int H = c->H;
   TRY(dalloc(c, &c->mod, (size_t)slots * T * c->n_mod * 4));
+  if (c->cand) TRY(dalloc(c, &c->fconst, (size_t)slots * T * 128 * 4));
   if (c->cfg.n_cross) TRY(dalloc(c, &c->modx, (size_t)slots * c->cfg.n_cross * T * 6 * H * 4));
   TRY(dalloc(c, &c->temb, (size_t)T * c->cfg.time_dim * e));
   TRY(dalloc(c, &c->th, (size_t)T * H * e));
@@ -1008,6 +1033,11 @@ dit_status prepare(dit_cache* c, int S, const void* text_emb, const std::vector<
       float* mod = c->mod + (size_t)slot * T * c->n_mod;
       g = lin_args(c, c->svec, H, c->M.mod, mod, c->n_mod, T, DIT_EPI_F32);
       TRY(gemm(c, &g, 1, cls));
+      if (c->fconst) {  // the reuse candidate's final-layer constants of every step
+        Scope s(c, cls, 0);
+        HIPCK(dit::launch_final_consts(mod, c->n_mod, c->n_mod - 2 * H, T, c->M.fin.w, c->M.fin.b, H,
+                                       c->fconst + (size_t)slot * T * 128, c->stream));
+      }
       if (c->cfg.n_cross) {
         const int base = 12 * H * c->cfg.n_double + 3 * H * c->cfg.n_single;
         for (int i = 0; i < c->cfg.n_cross; ++i) {
@@ -1116,10 +1146,14 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
 
   const bool pair = nb == 2;
   const bool unipc = p.solver == DIT_SOLVER_UNIPC;
-  // step: one fused launch per sample and step does the indicator and the
-  // reuse candidate (bf16, C = 64); fused: the older pair of fused kernels
-  const bool step = c->bf16 && dit::step_fused_fits(C, H, nb);
-  const bool fused = !step && c->bf16 && dit::reuse_fused_fits(C, H);
+  // sstream / step: the indicator and the reuse candidate of a sample and
+  // step come from one pass over its rows, before the decision (bf16, C = 64;
+  // sstream: the column-sliced kernels, step: the row-tiled fused kernel for
+  // widths they do not take); fused: the older pair of fused kernels
+  const bool sstream = c->cand != nullptr;
+  const bool step = !sstream && c->bf16 && dit::step_fused_fits(C, H, nb);
+  const bool spec_path = sstream || step;
+  const bool fused = !spec_path && c->bf16 && dit::reuse_fused_fits(C, H);
   const bool fused_euler = !pair && proj_fits(c) && !unipc;  // Euler folded into the projection
   const double thr = std::log(p.tau / (1.0 - p.tau));
   // mu(B, T) of the static policy: computed steps at floor(i T / B)
@@ -1167,7 +1201,7 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
       double* sums = c->sums_dev + 4 * j;
       const void* mp = t ? l.mbuf[l.i_prev] : nullptr;
       const void* ml = t ? l.mbuf[l.i_last] : nullptr;
-      if (step) {
+      if (spec_path) {
         // a step known to compute (t = 0, replay mask, spend-the-remainder,
         // static mask) writes h for the block stack instead of a reuse candidate
         bool known_full = t == 0;
@@ -1181,10 +1215,33 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
         Scope sc(c, DIT_K_INDICATOR, (double)NH * c->esz * (1 + reads + (l.spec ? nb : 1)));
         const float* mf0 = modp(j, 0, t) + (c->n_mod - 2 * H);
         const float* mf1 = pair ? modp(j, 1, t) + (c->n_mod - 2 * H) : nullptr;
-        HIPCK(dit::launch_step_fused(lat(j), C, c->M.img_in.w, c->M.img_in.b, l.mbuf[l.i_new], mp, ml, N, H, sh0, sc0,
-                                     t ? c->partials : nullptr, sums, l.spec ? l.r : nullptr, nb, c->M.fin.w,
-                                     c->M.fin.b, mf0, mf1, dsig, (float)p.guidance, unipc ? nullptr : alt[j],
-                                     unipc ? l.vspec : nullptr, l.spec ? nullptr : l.h, c->stream));
+        if (sstream) {
+          dit::StepStreamDesc d;
+          d.x = lat(j); d.rows = N; d.H = H;
+          d.W_in = c->M.img_in.w; d.b_in = c->M.img_in.b;
+          d.st_hi = c->st_hi; d.st_lo = c->st_lo; d.bbar = c->st_bbar; d.b2 = c->st_b2;
+          d.m_out = l.mbuf[l.i_new]; d.m_prev = mp; d.m_last = ml;
+          d.sh0 = sh0; d.sc0 = sc0;
+          // every step records sum |m_t|; later steps read the older buffers' sums from it
+          d.partials = c->partials; d.out = sums;
+          d.mag = l.mag; d.i_new = l.i_new; d.i_prev = l.i_prev; d.i_last = l.i_last;
+          if (l.spec) {
+            d.r = l.r; d.nb = nb;
+            d.W_out = c->M.fin.w; d.mf0 = mf0; d.mf1 = mf1;
+            d.fc0 = c->fconst + ((size_t)mod_slot(c, j, 0) * T + t) * 128;
+            d.fc1 = pair ? c->fconst + ((size_t)mod_slot(c, j, 1) * T + t) * 128 : nullptr;
+            d.cand = c->cand; d.dsig = dsig; d.guidance = (float)p.guidance;
+            d.x_spec = unipc ? nullptr : alt[j]; d.v_spec = unipc ? l.vspec : nullptr;
+          } else {
+            d.h_out = l.h;
+          }
+          HIPCK(dit::launch_step_stream(d, c->stream));
+        } else {
+          HIPCK(dit::launch_step_fused(lat(j), C, c->M.img_in.w, c->M.img_in.b, l.mbuf[l.i_new], mp, ml, N, H, sh0,
+                                       sc0, t ? c->partials : nullptr, sums, l.spec ? l.r : nullptr, nb, c->M.fin.w,
+                                       c->M.fin.b, mf0, mf1, dsig, (float)p.guidance, unipc ? nullptr : alt[j],
+                                       unipc ? l.vspec : nullptr, l.spec ? nullptr : l.h, c->stream));
+        }
       } else if (fused) {
         // embedding recomputed in LDS: reads m_{t-1} and m_{t_last} (once if equal), writes m_t
         Scope sc(c, DIT_K_INDICATOR, (double)NH * c->esz * (t == 0 ? 1 : (l.i_prev == l.i_last ? 2 : 3)));
@@ -1295,7 +1352,7 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
     for (int j = 0; j < S; ++j) {
       Lane& l = c->lanes[j];
       if (l.dec) continue;
-      if (step) {
+      if (spec_path) {
         // the candidate formed with the indicator is this step's result
         if (!l.spec) return fail_all(t, DIT_EINVAL, "internal: reused step without a reuse candidate");
         if (unipc) {
@@ -1334,14 +1391,22 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
 
     // (a4) full: the computing samples' block stacks, (a5) per sample
     if (!comp.empty()) {
-      if (step)  // the block stack's input h, unless the indicator launch already wrote it
+      if (spec_path)  // the block stack's input h, unless the indicator launch already wrote it
         for (int j : comp) {
           Lane& l = c->lanes[j];
           if (!l.spec) continue;
           Scope sc(c, DIT_K_FULL_OTHER, (double)NH * c->esz);
-          HIPCK(dit::launch_step_fused(lat(j), C, c->M.img_in.w, c->M.img_in.b, nullptr, nullptr, nullptr, N, H,
-                                       nullptr, nullptr, nullptr, nullptr, nullptr, nb, c->M.fin.w, c->M.fin.b,
-                                       nullptr, nullptr, 0.f, 0.f, nullptr, nullptr, l.h, c->stream));
+          if (sstream) {
+            dit::StepStreamDesc d;
+            d.x = lat(j); d.rows = N; d.H = H;
+            d.W_in = c->M.img_in.w; d.b_in = c->M.img_in.b;
+            d.h_out = l.h;
+            HIPCK(dit::launch_step_stream(d, c->stream));
+          } else {
+            HIPCK(dit::launch_step_fused(lat(j), C, c->M.img_in.w, c->M.img_in.b, nullptr, nullptr, nullptr, N, H,
+                                         nullptr, nullptr, nullptr, nullptr, nullptr, nb, c->M.fin.w, c->M.fin.b,
+                                         nullptr, nullptr, 0.f, 0.f, nullptr, nullptr, l.h, c->stream));
+          }
         }
       if (fused)  // the block stack's input h, bit-identical to the one the indicator used
         for (int j : comp) {
@@ -1449,6 +1514,7 @@ dit_status dit_cache_create(const dit_model_config* cfg, const void* weights, si
     if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
     if (e != hipSuccess) st = fail(c, DIT_EHIP, std::string("weight upload: ") + hipGetErrorString(e));
   }
+  if (st == DIT_OK && c->cand) st = upload_stream_stats(c, (const uint16_t*)weights);
   if (st != DIT_OK) {
     g_create_error = c->err;
     dit_cache_destroy(c);
@@ -1533,7 +1599,7 @@ void dit_cache_destroy(dit_cache* c) {
   free_per_call(c);
   for (Lane& l : c->lanes) free_lane(l);
   void* ps[] = {c->wdev, c->xs, c->X, c->A, c->Y, c->vt, c->modq, c->yf, c->vel, c->ctxkv, c->vt2, c->ones,
-                c->partials};
+                c->partials, c->cand, c->st_hi, c->st_lo};
   for (void* p : ps)
     if (p) hipFree(p);
   if (c->sums_host) hipHostFree(c->sums_host);

@@ -125,6 +125,50 @@ hipError_t launch_step_fused(const float* x, int C, const void* W_in, const void
                              const float* sc0, double* partials, double* out, const void* r, int nb,
                              const void* W_out, const void* b_out, const float* mf0, const float* mf1, float dsig,
                              float guidance, float* x_spec, float* v_spec, void* h_out, hipStream_t s);
+// Column-sliced form of the fused step (bf16, C = 64, H % 256 == 0): one
+// launch writes m_t (with partials != nullptr its sum |m| into mag[i_new]
+// and, with m_prev != nullptr, the four relative-L1 sums into out[4], the
+// magnitudes of m_prev and m_last read from mag[i_prev], mag[i_last]), h
+// (h_out != nullptr) and, with r != nullptr, per column slice the
+// reuse candidate's projection partials into `cand`; a second launch adds
+// the slices in a fixed order, applies the factored final LN, the guidance
+// combine and the Euler update (x + dsig v into x_spec, x unchanged) or
+// writes v into v_spec, and reduces the indicator partials.  The LN
+// statistics of h come from S(x) and the statistics matrix st_hi + st_lo
+// (step_stream_stats); fc_b = [A | B] of the branch (launch_final_consts).
+struct StepStreamDesc {
+  const float* x = nullptr; int rows = 0, H = 0;
+  const void* W_in = nullptr; const void* b_in = nullptr;
+  const void* st_hi = nullptr; const void* st_lo = nullptr; float bbar = 0.f, b2 = 0.f;
+  void* m_out = nullptr; const void* m_prev = nullptr; const void* m_last = nullptr;
+  const float* sh0 = nullptr; const float* sc0 = nullptr;
+  double* partials = nullptr; double* out = nullptr;
+  // sum |m| of each of the lane's three indicator buffers (device f64 [3]):
+  // the buffer written (i_new) and the two compared (i_prev, i_last)
+  double* mag = nullptr; int i_new = 0, i_prev = -1, i_last = -1;
+  const void* r = nullptr; int nb = 1;
+  const void* W_out = nullptr; const float* mf0 = nullptr; const float* mf1 = nullptr;
+  const float* fc0 = nullptr; const float* fc1 = nullptr;
+  float* cand = nullptr;
+  float dsig = 0.f, guidance = 1.f;
+  float* x_spec = nullptr; float* v_spec = nullptr;
+  void* h_out = nullptr;
+};
+bool step_stream_fits(int C, int H, int nb);
+// indicator partial 4-vectors and candidate partial floats one launch needs
+int step_stream_partials(int rows, int H);
+size_t step_stream_cand_floats(int rows, int H, int nb);
+// host: the [80][64] statistics matrix (centred Gram matrix of W_in's rows,
+// their mean, the bias-row cross term, zero rows) as bf16 hi + lo parts, the
+// bias mean and the bias's centred sum of squares; W_in [H][64], b_in [H] bf16.
+void step_stream_stats(const uint16_t* W_in, const uint16_t* b_in, int H, uint16_t* hi, uint16_t* lo, float* bbar,
+                       float* b2);
+hipError_t launch_step_stream(const StepStreamDesc& d, hipStream_t s);
+// out[row] = [A_c (64) | B_c (64)] for nrows rows of a modulation table
+// (shift at row * ld + off, scale H further): A_c = sum_k (1 + scale_k)
+// W_out[c, k], B_c = sum_k shift_k W_out[c, k] + b_out[c]; W_out [64][H] bf16.
+hipError_t launch_final_consts(const float* mod, int64_t ld, int off, int nrows, const void* W_out,
+                               const void* b_out, int H, float* out, hipStream_t s);
 // y = S(LN(S(a + b))(1+sc)+sh) per row (reuse-step final-layer input).
 template <typename T>
 hipError_t launch_add_ln_mod(const T* a, const T* b, T* out, int rows, int H, const float* sh,

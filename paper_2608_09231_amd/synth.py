@@ -150,6 +150,20 @@ WORKLOADS = {
            hidden=256, heads=2, head_dim=128, mlp_hidden=1024, in_channels=64,
            ctx_dim=96, n_img=512, n_txt=128),
         T=8, B=4, shift=3.0, guidance=1.0, seed=13),
+    # Shapes the column-sliced step kernel does not take (H not a multiple
+    # of 256; 32 latent channels): the row-tiled fused kernels run instead.
+    "small_w384_bf16": Workload(
+        "small_w384_bf16",
+        _m(name="small_w384_bf16", dtype="bf16", n_double=1, n_single=1, n_cross=0,
+           hidden=384, heads=3, head_dim=128, mlp_hidden=1536, in_channels=64,
+           ctx_dim=96, n_img=176, n_txt=40),
+        T=8, B=4, shift=3.0, guidance=1.0, seed=17),
+    "small_c32_bf16": Workload(
+        "small_c32_bf16",
+        _m(name="small_c32_bf16", dtype="bf16", n_double=1, n_single=1, n_cross=0,
+           hidden=256, heads=2, head_dim=128, mlp_hidden=1024, in_channels=32,
+           ctx_dim=96, n_img=184, n_txt=40),
+        T=8, B=4, shift=3.0, guidance=1.0, seed=19),
     "small_cross_bf16": Workload(
         "small_cross_bf16",
         _m(name="small_cross_bf16", dtype="bf16", n_double=0, n_single=0, n_cross=2,

@@ -99,6 +99,13 @@ def test_small_cross_bf16_parity():
     parity("small_cross_bf16")
 
 
+@pytest.mark.parametrize("name", ["small_w384_bf16", "small_c32_bf16"])
+def test_row_tiled_step_kernels_parity(name):
+    # widths and channel counts outside the column-sliced kernel's: the
+    # row-tiled fused kernels form the indicator and the reuse candidate
+    parity(name)
+
+
 def test_budget_edges_tiny():
     for T, B in ((1, 1), (6, 6), (7, 1)):
         parity("tiny", T=T, B=B)
