@@ -164,6 +164,20 @@ WORKLOADS = {
            hidden=256, heads=2, head_dim=128, mlp_hidden=1024, in_channels=32,
            ctx_dim=96, n_img=184, n_txt=40),
         T=8, B=4, shift=3.0, guidance=1.0, seed=19),
+    # Fewer image tokens than one 32-token tile of the column-sliced step
+    # kernel (a single ragged tile), single sample and guidance pair.
+    "micro_bf16": Workload(
+        "micro_bf16",
+        _m(name="micro_bf16", dtype="bf16", n_double=1, n_single=1, n_cross=0,
+           hidden=256, heads=2, head_dim=128, mlp_hidden=1024, in_channels=64,
+           ctx_dim=64, n_img=7, n_txt=5),
+        T=8, B=4, shift=3.0, guidance=1.0, seed=23),
+    "micro_cfg_bf16": Workload(
+        "micro_cfg_bf16",
+        _m(name="micro_cfg_bf16", dtype="bf16", n_double=2, n_single=0, n_cross=0,
+           hidden=512, heads=4, head_dim=128, mlp_hidden=2048, in_channels=64,
+           ctx_dim=64, n_img=33, n_txt=6, batch=2, pooled_text=False),
+        T=8, B=3, shift=3.0, guidance=4.0, seed=29),
     "small_cross_bf16": Workload(
         "small_cross_bf16",
         _m(name="small_cross_bf16", dtype="bf16", n_double=0, n_single=0, n_cross=2,

@@ -99,6 +99,13 @@ def test_small_cross_bf16_parity():
     parity("small_cross_bf16")
 
 
+@pytest.mark.parametrize("name", ["micro_bf16", "micro_cfg_bf16"])
+def test_fewer_tokens_than_one_tile(name):
+    # 7 image tokens (one ragged 32-token tile), and 33 (a full tile plus one
+    # token) as a guidance pair at H = 512 (four waves per work-group)
+    parity(name)
+
+
 @pytest.mark.parametrize("name", ["small_w384_bf16", "small_c32_bf16"])
 def test_row_tiled_step_kernels_parity(name):
     # widths and channel counts outside the column-sliced kernel's: the
