@@ -133,6 +133,8 @@ __global__ __launch_bounds__(64 * NW, (NB == 1 && NW == 4) ? 3 : 2) void step_st
   __shared__ float vec[2 + NB][SS_COLS * NW];  // 1 + scale0, shift0, then 1 + scale_f of each branch
   __shared__ __attribute__((aligned(16))) float stl[SS_TOK][8];  // per token: four Gram partials, s . wbar, s . g
   __shared__ float red[NW][4];
+  constexpr int XSW = SS_C + 8;  // bf16 per row of the S(x) tile (144 bytes: conflict-free fragment reads)
+  __shared__ __attribute__((aligned(16))) bf16_t xs[SS_TOK * XSW];
   __shared__ __attribute__((aligned(16))) char trb[NW][TRB];
   bf16_t* tr = (bf16_t*)trb[wave];
   float* cred = (float*)trb[wave];  // [SS_TOK][SS_PART] once the tile is done with
@@ -141,16 +143,21 @@ __global__ __launch_bounds__(64 * NW, (NB == 1 && NW == 4) ? 3 : 2) void step_st
   // Load order.  Vector loads return in issue order, so anything loaded after
   // the streamed rows would wait for them, and the compiler, left alone,
   // interleaves loads and waits to save registers.  Scheduling barriers pin
-  // the phases: (1) the L2-resident operands of the MFMA work (x, W_in and
-  // b_in, then, once x is converted, the statistics tiles and vectors);
+  // the phases: (1) the L2-resident operands of the MFMA work (x once per
+  // work-group, W_in and b_in, then, once S(x) is staged in LDS, the
+  // statistics tiles and vectors);
   // (2) the embedding and the statistics on MFMAs; (3) the indicator rows;
   // the residual rows follow as the first indicator rows are consumed, and
   // W_out once the candidate's operand is formed.
-  float xr[2][2][8];  // x of both token groups (MFMA layout)
+  // x of the 32 tokens, read once per work-group: 8-float chunks, chunk c =
+  // token c / 8, columns 8 (c % 8) .. + 7
+  constexpr int XC = SS_TOK * SS_C / 8 / (64 * NW);
+  float xr[XC][8];
 #pragma unroll
-  for (int g = 0; g < 2; ++g)
-#pragma unroll
-    for (int s = 0; s < 2; ++s) load_f8(a.x + crow(row0 + 16 * g + lr) * SS_C + 32 * s + 8 * lq, xr[g][s]);
+  for (int u = 0; u < XC; ++u) {
+    const int c = threadIdx.x + 64 * NW * u;
+    load_f8(a.x + crow(row0 + (c >> 3)) * SS_C + 8 * (c & 7), xr[u]);
+  }
   uint4 wi[4][2][2];  // W_in rows of the four tile pairs [pair][tile][k-block]
   uint4 bi[4];        // b_in of the lane's columns
 #pragma unroll
@@ -164,11 +171,11 @@ __global__ __launch_bounds__(64 * NW, (NB == 1 && NW == 4) ? 3 : 2) void step_st
     bi[p] = *(const uint4*)(a.b_in + colw + 32 * p + 8 * lq);
   }
   __builtin_amdgcn_sched_barrier(0);
-  uint4 xf[2][2];  // S(x): the B operand of every MFMA below (waits for x only)
 #pragma unroll
-  for (int g = 0; g < 2; ++g)
-#pragma unroll
-    for (int s = 0; s < 2; ++s) xf[g][s] = pack8(xr[g][s]);
+  for (int u = 0; u < XC; ++u) {  // S(x) into LDS (waits for x only)
+    const int c = threadIdx.x + 64 * NW * u;
+    *(uint4*)(xs + (c >> 3) * XSW + 8 * (c & 7)) = pack8(xr[u]);
+  }
   __builtin_amdgcn_sched_barrier(0);
   // statistics tiles of this wave (w, w + NW, ... < 5), hi and lo parts
   constexpr int NJ = (5 + NW - 1) / NW;
@@ -201,6 +208,12 @@ __global__ __launch_bounds__(64 * NW, (NB == 1 && NW == 4) ? 3 : 2) void step_st
     }
   __builtin_amdgcn_sched_barrier(0);
 
+  lds_barrier();  // the work-group's S(x) tile is in LDS
+  uint4 xf[2][2];  // S(x) fragments: the B operand of every MFMA below
+#pragma unroll
+  for (int g = 0; g < 2; ++g)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) xf[g][s] = *(const uint4*)(xs + (16 * g + lr) * XSW + 32 * s + 8 * lq);
   {
     // the embedding h = S(S(x) W_in^T + b_in): lane (lr, lq) of pair p ends
     // with h[token 16 g + lr][colw + 32 p + 8 lq + 0..7], stored to the tile
