@@ -490,15 +490,33 @@ struct CombineArgs {
 // Candidate combine (one work-group per 32 tokens: 8 threads per token, 8
 // output channels each; a token's slice partials are 264 contiguous bytes)
 // and the fixed-order reduction of the indicator partials into host-mapped
-// memory (the last work-group).
+// memory (the last work-group).  Both read their inputs in groups whose loads
+// are all issued before the first add (CB_SL slices, RD_U entries per
+// thread), clamped to the last valid index and discarded by a select; the
+// additions keep one thread's sequential order, so the result does not depend
+// on the group sizes.
 constexpr int CB_TOK = 32;
+constexpr int CB_SL = 6;
+constexpr int RD_U = 8;
 __global__ __launch_bounds__(256) void step_combine_kernel(CombineArgs a) {
   if ((int)blockIdx.x == a.cand_blocks) {
     __shared__ double sred[4][256];
     double acc[4] = {0, 0, 0, 0};
-    for (int i = threadIdx.x; i < a.n_ind; i += 256)
+    for (int i0 = threadIdx.x; i0 < a.n_ind; i0 += 256 * RD_U) {
+      double v[RD_U][4];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) acc[c] += a.ind_part[(int64_t)i * 4 + c];
+      for (int u = 0; u < RD_U; ++u) {
+        const double* q = a.ind_part + (int64_t)min(i0 + 256 * u, a.n_ind - 1) * 4;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) v[u][c] = q[c];
+      }
+#pragma unroll
+      for (int u = 0; u < RD_U; ++u) {
+        const bool ok = i0 + 256 * u < a.n_ind;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c] = ok ? acc[c] + v[u][c] : acc[c];
+      }
+    }
 #pragma unroll
     for (int c = 0; c < 4; ++c) sred[c][threadIdx.x] = acc[c];
     __syncthreads();
@@ -526,28 +544,40 @@ __global__ __launch_bounds__(256) void step_combine_kernel(CombineArgs a) {
   const int tl = threadIdx.x >> 3, c0 = 8 * (threadIdx.x & 7);
   const int tok = blockIdx.x * CB_TOK + tl;
   if (tok >= a.rows) return;
+  const int64_t o = (int64_t)tok * SS_C + c0;
+  float xv[8];
+  if (!a.v_spec) load_f8(a.x + o, xv);
   const float invH = 1.f / (float)a.H;
+  const int64_t sstride = (int64_t)a.ntile * SS_TOK * SS_PART;
   float vres[8];
   for (int b = 0; b < a.nb; ++b) {
     const float* base = a.cand + ((int64_t)b * a.nsl * a.ntile * SS_TOK + tok) * SS_PART;
-    const int64_t sstride = (int64_t)a.ntile * SS_TOK * SS_PART;
-    float P[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    float D1 = 0.f, D2 = 0.f;
-    for (int sl = 0; sl < a.nsl; ++sl) {
-      const float* q = base + sl * sstride;
-      float v[8];
-      load_f8(q + c0, v);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) P[e] += v[e];
-      D1 += q[64];
-      D2 += q[65];
-    }
-    const float dm = D1 * invH;
-    const float rho = rsqrtf(fmaxf(D2 * invH - dm * dm, 0.f) + DIT_LN_EPS);
     const float* fc = b ? a.fc1 : a.fc0;
     float A[8], B[8];
     load_f8(fc + c0, A);
     load_f8(fc + SS_C + c0, B);
+    float P[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float D1 = 0.f, D2 = 0.f;
+    for (int s0 = 0; s0 < a.nsl; s0 += CB_SL) {
+      float v[CB_SL][8];
+      float2 dd[CB_SL];
+#pragma unroll
+      for (int u = 0; u < CB_SL; ++u) {
+        const float* q = base + min(s0 + u, a.nsl - 1) * sstride;
+        load_f8(q + c0, v[u]);
+        dd[u] = *(const float2*)(q + 64);
+      }
+#pragma unroll
+      for (int u = 0; u < CB_SL; ++u) {
+        const bool ok = s0 + u < a.nsl;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) P[e] = ok ? P[e] + v[u][e] : P[e];
+        D1 = ok ? D1 + dd[u].x : D1;
+        D2 = ok ? D2 + dd[u].y : D2;
+      }
+    }
+    const float dm = D1 * invH;
+    const float rho = rsqrtf(fmaxf(D2 * invH - dm * dm, 0.f) + DIT_LN_EPS);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float v = rho * (P[e] - dm * A[e]) + B[e];
@@ -555,13 +585,10 @@ __global__ __launch_bounds__(256) void step_combine_kernel(CombineArgs a) {
       vres[e] = b == 0 ? v : v + a.guidance * (vres[e] - v);
     }
   }
-  const int64_t o = (int64_t)tok * SS_C + c0;
   if (a.v_spec) {
     *(float4*)(a.v_spec + o) = make_float4(vres[0], vres[1], vres[2], vres[3]);
     *(float4*)(a.v_spec + o + 4) = make_float4(vres[4], vres[5], vres[6], vres[7]);
   } else {
-    float xv[8];
-    load_f8(a.x + o, xv);
     *(float4*)(a.x_spec + o) = make_float4(xv[0] + a.dsig * vres[0], xv[1] + a.dsig * vres[1],
                                            xv[2] + a.dsig * vres[2], xv[3] + a.dsig * vres[3]);
     *(float4*)(a.x_spec + o + 4) = make_float4(xv[4] + a.dsig * vres[4], xv[5] + a.dsig * vres[5],
