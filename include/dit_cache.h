@@ -129,7 +129,8 @@ enum { DIT_SOLVER_EULER = 0, DIT_SOLVER_UNIPC = 1 };
 typedef struct dit_sample_params {
   int32_t T;                    /* steps, >= 1 */
   int32_t B;                    /* full evaluations, 1 <= B <= T */
-  const double* sigmas;         /* host [T+1] with sigma_0 = 1 > ... > sigma_T = 0, or NULL */
+  const double* sigmas;         /* host [T+1] in [0, 1], strictly decreasing (the default schedule
+                                   runs from sigma_0 = 1 to sigma_T = 0), or NULL; else DIT_EINVAL */
   double shift;                 /* used when sigmas == NULL: sigma_i = s u / (1 + (s-1) u), u = 1 - i/T */
   double tau;                   /* cutoff on sigma(z), in (0, 1); the paper uses 0.5 */
   double guidance;              /* guidance scale g, used when batch == 2 */

@@ -170,10 +170,30 @@ class DitCache:
         except Exception:
             pass
 
+    def _check_io(self, latents, text_embs, S):
+        """The library reads S x [N, C] f32 latents and S x [batch, N_t, ctx]
+        text embeddings in the storage dtype through raw device pointers:
+        check that the tensors hold exactly that."""
+        cfg = self.cfg
+        esz = 2 if cfg.dtype == "bf16" else 4
+        for t, name, n, size in ((latents, "latent", S * cfg.n_img * cfg.in_channels, 4),
+                                 (text_embs, "text_emb", S * cfg.batch * cfg.n_txt * cfg.ctx_dim, esz)):
+            if not getattr(t, "is_cuda", False):
+                raise ValueError(f"{name} must be a device tensor")
+            if not t.is_contiguous() or t.numel() != n or t.element_size() != size:
+                raise ValueError(f"{name} must be contiguous with {n} elements of {size} bytes")
+        if not latents.is_floating_point():
+            raise ValueError("latent must be float32")
+
     @staticmethod
-    def _params(T, B, sigmas, shift, tau, guidance, forced_mask, indicator, policy, delta, solver):
+    def _params(T, B, sigmas, shift, tau, guidance, forced_mask, indicator, policy, delta, solver, S=1):
         sig = None if sigmas is None else np.ascontiguousarray(sigmas, np.float64)
         fm = None if forced_mask is None else np.ascontiguousarray(forced_mask, np.uint8)
+        # the library reads T + 1 sigmas and T mask entries per sample
+        if sig is not None and sig.size != int(T) + 1:
+            raise ValueError(f"sigmas must hold T + 1 = {int(T) + 1} values")
+        if fm is not None and fm.size != S * int(T):
+            raise ValueError(f"forced mask must hold {S} x T = {S * int(T)} entries")
         p = SampleParamsC(int(T), int(B),
                           sig.ctypes.data_as(C.POINTER(C.c_double)) if sig is not None else None,
                           float(shift), float(tau), float(guidance),
@@ -214,6 +234,7 @@ class DitCache:
         or torch.bfloat16); policy "gate" | "static" | "threshold" (the
         latter two do not read gate_blob, which may be None); solver
         "euler" | "unipc"."""
+        self._check_io(latent, text_emb, 1)
         gate = np.ascontiguousarray(gate_blob if gate_blob is not None else [], np.float32)
         arrs, cs = self._schedules(1, T)
         p, keep = self._params(T, B, sigmas, shift, tau, guidance, forced_mask, indicator, policy, delta, solver)
@@ -237,10 +258,11 @@ class DitCache:
             raise ValueError("latents and text_embs disagree on the number of samples")
         if forced_masks is not None and np.shape(forced_masks) != (S, T):
             raise ValueError("forced_masks must be [n_samples, T]")
+        self._check_io(latents, text_embs, S)
         gate = np.ascontiguousarray(gate_blob if gate_blob is not None else [], np.float32)
         arrs, cs = self._schedules(S, T)
         p, keep = self._params(T, B, sigmas, shift, tau, guidance, forced_masks, indicator, policy, delta,
-                               solver)
+                               solver, S)
         st = _lib.dit_cache_sample_batch(self._h, S, C.c_void_p(latents.data_ptr()),
                                          C.c_void_p(text_embs.data_ptr()),
                                          gate.ctypes.data_as(C.c_void_p) if gate.size else None, gate.size,

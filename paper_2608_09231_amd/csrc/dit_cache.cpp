@@ -1542,6 +1542,13 @@ dit_status dit_cache_sample_batch(dit_cache* c, int32_t n_samples, float* latent
   if (p->indicator != DIT_INDICATOR_MODULATED && p->indicator != DIT_INDICATOR_PATCH)
     return fail(c, DIT_EINVAL, "bad indicator");
   if (!p->sigmas && !(p->shift > 0.0)) return fail(c, DIT_EINVAL, "shift must be > 0");
+  if (p->sigmas)
+    for (int i = 0; i <= p->T; ++i) {
+      const double s = p->sigmas[i];
+      // NaN fails every comparison; equal neighbours would make the UniPC step size zero
+      if (!(s >= 0.0 && s <= 1.0) || (i > 0 && !(s < p->sigmas[i - 1])))
+        return fail(c, DIT_EINVAL, "sigmas must lie in [0, 1] and decrease strictly");
+    }
   if (p->policy != DIT_POLICY_GATE && p->policy != DIT_POLICY_STATIC && p->policy != DIT_POLICY_THRESHOLD)
     return fail(c, DIT_EINVAL, "bad policy");
   if (p->solver != DIT_SOLVER_EULER && p->solver != DIT_SOLVER_UNIPC) return fail(c, DIT_EINVAL, "bad solver");

@@ -703,11 +703,14 @@ void step_stream_stats(const uint16_t* W_in, const uint16_t* b_in, int H, uint16
 hipError_t launch_step_stream(const StepStreamDesc& d, hipStream_t s) {
   const int nw = stream_waves(d.H);
   if (!step_stream_fits(SS_C, d.H, d.nb) || d.rows < 1) return hipErrorInvalidValue;
+  // the embedding runs on every launch; the modulation is a shift and a scale together
+  if (!d.x || !d.W_in || !d.b_in || (d.sh0 == nullptr) != (d.sc0 == nullptr) || (d.m_prev && !d.m_last))
+    return hipErrorInvalidValue;
   // sums need m_t and the magnitude record; differences need the sums and the host-mapped output
   if ((d.partials && (!d.m_out || !d.mag || d.i_new < 0 || d.i_new > 2)) ||
       (d.m_prev && (!d.partials || !d.out || d.i_prev < 0 || d.i_prev > 2 || d.i_last < 0 || d.i_last > 2)))
     return hipErrorInvalidValue;
-  if (d.r && (!d.cand || !d.fc0 || (d.nb == 2 && (!d.fc1 || !d.mf1)) || !d.mf0 || (!d.x_spec && !d.v_spec)))
+  if (d.r && (!d.cand || !d.W_out || !d.fc0 || (d.nb == 2 && (!d.fc1 || !d.mf1)) || !d.mf0 || (!d.x_spec && !d.v_spec)))
     return hipErrorInvalidValue;
   if ((d.m_out || d.r) && (!d.st_hi || !d.st_lo)) return hipErrorInvalidValue;
   const int nsl = d.H / (SS_COLS * nw), ntile = (d.rows + SS_TOK - 1) / SS_TOK;

@@ -244,6 +244,18 @@ def test_error_paths_on_device():
     with pytest.raises(binding.DitError) as e:
         h.sample(lat, txt, None, 5, 2, policy="threshold", delta=float("nan"))
     assert e.value.status == binding.DIT_EINVAL
+    # the binding refuses buffers of the wrong size before the library reads them
+    for kw in ({"sigmas": np.linspace(1.0, 0.0, 5)}, {"forced_mask": [1, 1, 0, 0]}):
+        with pytest.raises(ValueError):
+            h.sample(lat, txt, gate, 5, 2, **kw)
+    for a, b in ((lat[:-1], txt), (lat.double(), txt), (lat, txt[:, :-1]), (lat.cpu(), txt)):
+        with pytest.raises(ValueError):
+            h.sample(a, b, gate, 5, 2)
+    good = np.linspace(1.0, 0.0, 6)
+    for sig in (good[::-1].copy(), np.r_[good[:3], good[2:5]], np.r_[1.5, good[1:]], np.r_[good[:5], np.nan]):
+        with pytest.raises(binding.DitError) as e:
+            h.sample(lat, txt, gate, 5, 2, sigmas=sig)
+        assert e.value.status == binding.DIT_EINVAL
     bad = lat.clone()
     bad[3, 2] = float("nan")
     with pytest.raises(binding.DitError) as e:
