@@ -32,7 +32,8 @@ enum {
  *   A    device bf16 [M, K], row stride lda elements (lda >= K, K % 8 == 0)
  *   W    device bf16 [N, K], row stride ldw (torch nn.Linear layout)
  *   bias device bf16 [N] or NULL
- *   C    device bf16 (f32 with DIT_EPI_F32) [M, *], row stride ldc
+ *   C    device bf16 (f32 with DIT_EPI_F32) [M, *], row stride ldc (>= N,
+ *        plus gap when gap_at < N; else DIT_ESHAPE)
  *   gate device f32 [N], DIT_EPI_GATED_RES only
  *   rms_cols  columns n < rms_cols are normalised per 128-wide head
  *             (RMS, eps 1e-6, unit gain) before rounding; 0 = none;
@@ -41,8 +42,8 @@ enum {
  *   gap_at, gap  output column = n + gap for n >= gap_at (writes the MLP
  *             half of a fused projection next to a hole for the attention
  *             output); gap = 0 = none
- * Errors: DIT_EINVAL (null pointers, bad flags), DIT_ESHAPE (K % 8, lda <
- * K, rms_cols not a multiple of 128), DIT_EHIP. */
+ * Errors: DIT_EINVAL (null pointers, bad flags), DIT_ESHAPE (K % 8, lda or
+ * ldw < K, ldc too small, gap < 0, rms_cols not a multiple of 128), DIT_EHIP. */
 typedef struct dit_gemm_desc {
   const void* A; int64_t lda;
   const void* W; int64_t ldw;

@@ -1644,8 +1644,11 @@ dit_status dit_gemm_bf16(const dit_gemm_desc* d, void* hip_stream) {
   if (d->flags & ~(DIT_EPI_F32 | DIT_EPI_GATED_RES | DIT_EPI_SILU)) return fail(c, DIT_EINVAL, "bad flags");
   if ((d->flags & DIT_EPI_GATED_RES) && (!d->gate || (d->flags & DIT_EPI_F32)))
     return fail(c, DIT_EINVAL, "gated residual needs a gate and bf16 output");
-  if (d->M < 0 || d->N < 0 || d->K < 1 || d->K % 8 || d->lda < d->K || d->ldw < d->K)
+  if (d->M < 0 || d->N < 0 || d->K < 1 || d->K % 8 || d->lda < d->K || d->ldw < d->K || d->gap < 0)
     return fail(c, DIT_ESHAPE, "bad GEMM shape");
+  // the last output column is N - 1, plus the gap when it lies past gap_at
+  if (d->ldc < (int64_t)d->N + (d->gap && d->gap_at < d->N ? d->gap : 0))
+    return fail(c, DIT_ESHAPE, "ldc is smaller than the output row");
   if (d->rms_cols < 0 || d->rms_cols % 128) return fail(c, DIT_ESHAPE, "rms_cols must be a multiple of 128");
   GemmArgs g{};
   g.A = d->A; g.lda = d->lda; g.W = d->W; g.ldw = d->ldw; g.bias = d->bias;

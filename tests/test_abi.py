@@ -91,6 +91,27 @@ def test_noalloc_attention_rejects_oversized_on_the_host():
     assert st == binding.DIT_EINVAL
 
 
+def test_gemm_rejects_bad_shapes_on_the_host():
+    """The GEMM entry point checks its shape and strides before any device
+    call (no GPU needed; nothing is launched)."""
+    lib = binding.load()
+    fake = 0x1000
+
+    def desc(**kw):
+        d = dict(A=fake, lda=256, W=fake, ldw=256, bias=None, C=fake, ldc=512, M=64, N=512, K=256,
+                 flags=0, gate=None, rms_cols=0, gelu_from=512, gap_at=0, gap=0)
+        d.update(kw)
+        return binding.GemmDescC(**d)
+
+    for kw in ({"K": 250, "lda": 256, "ldw": 256}, {"lda": 128}, {"ldw": 128}, {"ldc": 511},
+               {"ldc": 600, "gap_at": 256, "gap": 128}, {"gap": -1}, {"rms_cols": 100}):
+        d = desc(**kw)
+        assert lib.dit_gemm_bf16(C.byref(d), None) == binding.DIT_ESHAPE, kw
+    for kw in ({"flags": 8}, {"flags": binding.EPI_GATED_RES}, {"C": None}):
+        d = desc(**kw)
+        assert lib.dit_gemm_bf16(C.byref(d), None) == binding.DIT_EINVAL, kw
+
+
 # ---------------------------------------------------------------- host gate
 
 def _gates():
