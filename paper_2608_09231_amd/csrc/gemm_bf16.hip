@@ -8,12 +8,10 @@
 // ((row >> 1) & 7): two consecutive 128-byte rows fill one 256-byte bank
 // cycle, so the fragment reads of 16 consecutive rows hit 16 distinct 16-byte
 // bank groups.  The main kernel (256 x 256 tiles, 8 waves of 64 x 128) keeps
-// a ring of five operand slices in LDS so A slices arrive two slices ahead;
-// smaller tiles use a two-stage pipeline.  Workgroups are remapped so that
-// each of the 8 XCDs walks a contiguous, M-grouped range of tiles (its own L2
-// sees the shared A rows / W columns).
-#include <stdlib.h>
-
+// a ring of five operand slices in LDS: W slices (cold, from HBM) arrive two
+// slices ahead of use, A slices one; smaller tiles use a two-stage pipeline.
+// Workgroups are remapped so that each of the 8 XCDs walks a contiguous,
+// M-grouped range of tiles (its own L2 sees the shared A rows / W columns).
 #include <type_traits>
 #include <utility>
 
