@@ -81,6 +81,11 @@ struct Lane {
   float* xalt = nullptr;    // f32 [N, C]: second latent buffer (the reuse candidate's Euler result)
   float* vspec = nullptr;   // f32 [N, C]: the reuse candidate's velocity (UniPC)
   double* mag = nullptr;    // f64 [3]: sum |m| of each indicator buffer (column-sliced step kernel)
+  // video blocks: the cross-attention keys | values of the text tokens [nb, n_cross, Nt, 2H] and (bf16)
+  // the values transposed [nb, n_cross, heads, 128, round_up(Nt, 64)]; the same at every step, so
+  // formed once per sample
+  void* xkv = nullptr;
+  void* xvt = nullptr;
   int cnt = 0, t_last = 0, i_prev = -1, i_last = -1, i_new = 0;
   double acc = 0.0;
   bool dec = true;
@@ -115,8 +120,6 @@ struct dit_cache {
   float* modq = nullptr;   // f32 [cap_seq, n_mod]: gathered modulation vectors of one step
   void* yf = nullptr;      // [N, H] final-layer input
   float* vel = nullptr;    // f32 [nb, N, C]
-  void* ctxkv = nullptr;   // [Nt, 2H] cross-attention k | v
-  void* vt2 = nullptr;     // bf16 [heads, 128, round_up(Nt, 64)]
   float* ones = nullptr;   // f32 [H] (ungated residual)
   double* partials = nullptr;
   int max_partials = 0;
@@ -413,9 +416,13 @@ dit_status upload_stream_stats(dit_cache* c, const uint16_t* blob) {
   return DIT_OK;
 }
 
+// Per video block: the text tokens' keys | values, and the values transposed.
+size_t xkv_elems(const dit_cache* c) { return (size_t)c->Nt * 2 * c->H; }
+size_t xvt_elems(const dit_cache* c) { return (size_t)c->cfg.heads * 128 * rup(c->Nt, 64); }
+
 void free_lane(Lane& l) {
   void* ps[] = {l.h, l.mbuf[0], l.mbuf[1], l.mbuf[2], l.r, l.txt, l.x_last, l.mh[0], l.mh[1], l.mh[2],
-                l.xalt, l.vspec, l.mag};
+                l.xalt, l.vspec, l.mag, l.xkv, l.xvt};
   for (void* p : ps)
     if (p) hipFree(p);
   l = Lane{};
@@ -433,6 +440,11 @@ dit_status alloc_lane(dit_cache* c, Lane& l) {
   TRY(dalloc(c, &l.xalt, NC * 4));
   TRY(dalloc(c, &l.vspec, NC * 4));
   TRY(dalloc(c, &l.mag, 3 * sizeof(double)));
+  if (c->cfg.n_cross) {
+    const size_t nblk = (size_t)c->nb * c->cfg.n_cross;
+    TRY(dalloc(c, &l.xkv, nblk * xkv_elems(c) * e));
+    if (c->bf16) TRY(dalloc(c, &l.xvt, nblk * xvt_elems(c) * 2));
+  }
   return DIT_OK;
 }
 
@@ -491,10 +503,6 @@ dit_status alloc_workspace(dit_cache* c) {
   TRY(dalloc(c, &c->xs, (size_t)N * c->C * e));
   TRY(dalloc(c, &c->yf, (size_t)N * H * e));
   TRY(dalloc(c, &c->vel, (size_t)c->nb * N * c->C * 4));
-  if (c->cfg.n_cross) {
-    TRY(dalloc(c, &c->ctxkv, (size_t)Nt * 2 * H * e));
-    if (c->bf16) TRY(dalloc(c, &c->vt2, (size_t)c->cfg.heads * 128 * rup(Nt, 64) * 2));
-  }
   TRY(dalloc(c, &c->ones, (size_t)H * 4));
   {
     std::vector<float> one(H, 1.f);
@@ -661,6 +669,8 @@ struct Seq {
   const float* mod;   // this step's modulation vector [n_mod]
   const float* modx;  // video blocks: base of [n_cross][T][6H]
   const void* m0;     // [N, H] the first block's modulated image input (m_t), or nullptr
+  const void* xkv;    // video blocks: this branch's [n_cross, Nt, 2H] text keys | values
+  void* xvt;          // bf16 video blocks: [n_cross, ...] the values transposed
 };
 
 // One sequence at a time (f32 storage, video blocks).
@@ -704,12 +714,12 @@ dit_status full_stack(dit_cache* c, const Seq& q, int t, int T) {
       TRY(ln_mod(c, c->X, H, c->A, H, N, N, nullptr, nullptr, nullptr, nullptr, DIT_K_FULL_OTHER));
       GemmArgs gq = lin_args(c, c->A, H, w.xq, c->Y, ldY, N);
       gq.rms_cols = H;
-      GemmArgs gkv = lin_args(c, q.txt, H, w.xkv, c->ctxkv, 2 * H, Nt);
-      gkv.rms_cols = H;
       TRY(gemm(c, &gq, 1, cls));
-      TRY(gemm(c, &gkv, 1, cls));
-      TRY(attention(c, c->Y, ldY, c->ctxkv, 2 * H, sp(c, c->ctxkv, H), 2 * H, sp(c, c->Y, 3 * H), ldY, N, Nt,
-                    c->bf16 ? c->vt2 : nullptr));
+      // the text tokens' keys and values (and the transposed values) were formed once for the sample
+      const char* kv = sp(c, q.xkv, (size_t)i * xkv_elems(c));
+      void* vt = c->bf16 ? (void*)((char*)q.xvt + (size_t)i * xvt_elems(c) * 2) : nullptr;
+      TRY(attention(c, c->Y, ldY, kv, 2 * H, kv + (size_t)H * c->esz, 2 * H, sp(c, c->Y, 3 * H), ldY, N, Nt, vt,
+                    0x7fffffff, 0, 1, 0, 0, c->bf16));
       g = lin_args(c, sp(c, c->Y, 3 * H), ldY, w.xo, c->X, H, N, DIT_EPI_GATED_RES);
       g.gate = c->ones;
       TRY(gemm(c, &g, 1, cls));
@@ -1006,6 +1016,19 @@ dit_status prepare(dit_cache* c, int S, const void* text_emb, const std::vector<
       const void* te = (const char*)text_emb + ((size_t)j * c->nb + b) * Nt * X * c->esz;
       g = lin_args(c, te, X, c->M.txt_in, sp(c, c->lanes[j].txt, (size_t)b * Nt * H), H, Nt);
       TRY(gemm(c, &g, 1, cls));
+      for (int i = 0; i < c->cfg.n_cross; ++i) {  // every video block's text keys | values (rms-normed k)
+        const Lane& l = c->lanes[j];
+        const size_t bi = (size_t)b * c->cfg.n_cross + i;
+        char* kv = sp(c, l.xkv, bi * xkv_elems(c));
+        GemmArgs gkv = lin_args(c, sp(c, l.txt, (size_t)b * Nt * H), H, c->M.crs[i].xkv, kv, 2 * H, Nt);
+        gkv.rms_cols = H;
+        TRY(gemm(c, &gkv, 1, cls));
+        if (c->bf16) {
+          Scope s(c, cls, 0);
+          HIPCK(dit::launch_transpose_v_bf16(kv + (size_t)H * 2, 2 * H, (char*)l.xvt + bi * xvt_elems(c) * 2, Nt,
+                                             c->cfg.heads, c->stream));
+        }
+      }
       if ((j > 0 || b > 0) && !c->cfg.pooled_text) continue;  // identical vec and mod table
       const int slot = mod_slot(c, j, b);
       const float* pvp = nullptr;
@@ -1420,8 +1443,10 @@ dit_status run_batch(dit_cache* c, int S, float* latents, const void* text_emb, 
           Lane& l = c->lanes[j];
           // the indicator tensor is the first block's modulated image input of branch 0
           const void* m0 = (p.indicator == DIT_INDICATOR_MODULATED && b == 0) ? l.mbuf[l.i_new] : nullptr;
+          const size_t nx = (size_t)b * c->cfg.n_cross;
           seqs.push_back(Seq{sp(c, l.txt, (size_t)b * c->Nt * H), l.h, sp(c, l.r, b * NH), modp(j, b, t),
-                             modxp(j, b), m0});
+                             modxp(j, b), m0, l.xkv ? sp(c, l.xkv, nx * xkv_elems(c)) : nullptr,
+                             l.xvt ? (char*)l.xvt + nx * xvt_elems(c) * 2 : nullptr});
         }
       const int Q = (int)seqs.size();
       if (c->stacked) TRY(full_stack_multi(c, seqs.data(), Q));
@@ -1605,7 +1630,7 @@ void dit_cache_destroy(dit_cache* c) {
   if (c->stream) hipStreamSynchronize(c->stream);
   free_per_call(c);
   for (Lane& l : c->lanes) free_lane(l);
-  void* ps[] = {c->wdev, c->xs, c->X, c->A, c->Y, c->vt, c->modq, c->yf, c->vel, c->ctxkv, c->vt2, c->ones,
+  void* ps[] = {c->wdev, c->xs, c->X, c->A, c->Y, c->vt, c->modq, c->yf, c->vel, c->ones,
                 c->partials, c->cand, c->st_hi, c->st_lo};
   for (void* p : ps)
     if (p) hipFree(p);
