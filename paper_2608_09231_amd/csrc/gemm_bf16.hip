@@ -878,7 +878,6 @@ __global__ __launch_bounds__(256) void proj_small_n_kernel(const bf16_t* __restr
   for (int j = 0; j < NT; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const bf16_t* ap = A + (int64_t)row * lda + 8 * lq;
   const bf16_t* wp = W + (int64_t)lr * ldw + 8 * lq;
-#pragma unroll 4
   for (int st = s0; st < s1; ++st) {
     const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *(const uint4*)(ap + 32 * st));
 #pragma unroll
