@@ -62,6 +62,62 @@ def test_flux1024_two_blocks_each():
     reduced_parity("flux1024", T=3, B=2, n_double=2, n_single=2)
 
 
+# The displacement x_T - x_0 is held to the latents' own bar: the device
+# rounds to bf16 at the points where the oracle does, so the two differ only
+# where f32 and f64 accumulation round a value to neighbouring bf16 numbers.
+DX_TOL = 2e-2
+
+
+def _golden_result(g):
+    """The stored oracle run as the fields the schedule and logit checks read."""
+    import types
+    f64 = lambda rows: np.array([[np.nan if v is None else v for v in np.atleast_1d(r)] for r in rows],
+                                np.float64)
+    return types.SimpleNamespace(full=np.array(g["full"], np.uint8), forced=np.array(g["forced"], np.uint8),
+                                 logit=f64(g["logit"]).ravel(), nfe=int(g["nfe"]), features=f64(g["features"]),
+                                 sums=f64(g["sums"]))
+
+
+def test_flux1024_full_depth_against_oracle_golden():
+    """FLUX-1024 at its full depth (19 double + 38 single blocks, full widths
+    and token counts) against the oracle's own gated run on T = 4, B = 2,
+    stored by tests/golden/make_flux1024_full_depth.py (the float64 oracle
+    needs about 40 minutes for it): decisions and logits by the margin
+    protocol, then the final latent and its displacement x_T - x_0 on every
+    256th element, and their norms."""
+    import json
+    import os
+    torch = torch_cuda()
+    with open(os.path.join(os.path.dirname(__file__), "golden", "flux1024_full_depth.json")) as f:
+        g = json.load(f)
+    w = synth.reduced(synth.workload("flux1024"), T=g["T"], B=g["B"], name="flux1024_full_depth")
+    assert (w.model.n_double, w.model.n_single, w.shift, w.seed, w.solver) == \
+        (g["n_double"], g["n_single"], g["shift"], g["seed"], g["solver"])
+    t0 = time.time()
+    weights, x0, text, gate = synth.make_inputs(w)
+    x_gpu, sched, h = run_sampler(torch, w, weights, x0, text, gate, solver=w.solver)
+    h.close()
+    del weights
+    say(f"{w.name}: device schedule {sched.full.tolist()}, golden {g['full']} ({time.time() - t0:.1f} s)")
+    ores = _golden_result(g)
+    check_schedule_against_oracle(sched, ores)
+    check_logits(sched, ores, gate)
+    # every gated decision of the stored run is far from the cutoff, so the
+    # device takes the same path and the latents are comparable
+    assert (sched.full == ores.full).all()
+    k = int(g["stride"])
+    x = x_gpu.ravel()
+    dx = x - np.asarray(x0, np.float64).ravel()
+    err = rel_l2(x[::k], g["x_sample"])
+    err_dx = rel_l2(dx[::k], g["dx_sample"])
+    say(f"{w.name}: latent rel-L2 {err:.3e} (sampled), displacement rel-L2 {err_dx:.3e}, "
+        f"norms {np.linalg.norm(x):.6e} / {g['x_norm']:.6e}, {np.linalg.norm(dx):.6e} / {g['dx_norm']:.6e}")
+    assert err <= 2e-2
+    assert abs(np.linalg.norm(x) - g["x_norm"]) <= 2e-2 * g["x_norm"]
+    assert err_dx <= DX_TOL
+    assert abs(np.linalg.norm(dx) - g["dx_norm"]) <= DX_TOL * g["dx_norm"]
+
+
 def test_flux2048_full_tokens_one_block_each():
     """FLUX-2048 at its real token count (16384 image + 512 text tokens): one
     computed and one reused step through one double and one single block."""
