@@ -1,0 +1,89 @@
+"""Write the full-size oracle goldens of tests/golden/:
+
+  flux1024_full_depth.json  FLUX-1024 at its full depth (19 double + 38 single
+                            blocks, H 3072, 4096 image + 512 text tokens),
+                            T = 4, B = 2: two passes through the whole block
+                            stack, two residual reuses (about 36 minutes);
+  wan14b_full_tokens.json   the Wan block at its full width and token count
+                            (one video block, H 5120, 32760 video tokens, 512
+                            text tokens) with the workload's UniPC step rule,
+                            T = 3, B = 2 (about 25 minutes).
+
+The float64 oracle needs about 17-21 s per full-width FLUX block and about six
+minutes per Wan block at 32760 tokens on eight host cores, so these runs are
+stored rather than recomputed by the GPU tests.
+
+Stored per case: the schedule, the gate logits, forced flags, state features
+and indicator sums of every step, the final latent x_T and the displacement
+x_T - x_0 at every 256th element (values of each), and their full L2 norms.
+Only the oracle and the seeded input generators are called.  Run from the
+repository root (no argument: every case):
+    python tests/golden/make_full_size_goldens.py [case ...]
+"""
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+sys.path.insert(0, ROOT)
+
+from oracle import sample  # noqa: E402
+from paper_2608_09231_amd import synth  # noqa: E402
+
+STRIDE = 256
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+# case -> (workload, reduction of synth.reduced)
+CASES = {
+    "flux1024_full_depth": ("flux1024", dict(T=4, B=2)),
+    "wan14b_full_tokens": ("wan14b", dict(T=3, B=2, n_cross=1)),
+}
+
+
+def workload(case):
+    """The seeded workload of a case (shared with the GPU tests)."""
+    name, kw = CASES[case]
+    return synth.reduced(synth.workload(name), name=case, **kw)
+
+
+def _nan_to_none(a):
+    return [None if not np.isfinite(v) else float(v) for v in np.asarray(a, np.float64).ravel()]
+
+
+def make(case):
+    w = workload(case)
+    cfg = w.model
+    t0 = time.time()
+    weights, x0, text, gate = synth.make_inputs(w)
+    print(f"{case}: inputs ready ({time.time() - t0:.0f} s)", flush=True)
+    res = sample(cfg, weights.tensors, gate, x0, text, w.T, w.B, shift=w.shift, guidance=w.guidance,
+                 solver=w.solver)
+    print(f"{case}: oracle done ({time.time() - t0:.0f} s): schedule {res.full.tolist()}", flush=True)
+    x = np.asarray(res.x, np.float64).ravel()
+    dx = x - np.asarray(x0, np.float64).ravel()
+    out = {
+        "note": f"oracle (float64) gated sample of {case}; written by tests/golden/make_full_size_goldens.py",
+        "workload": CASES[case][0], "n_double": cfg.n_double, "n_single": cfg.n_single,
+        "n_cross": cfg.n_cross, "n_img": cfg.n_img,
+        "T": w.T, "B": w.B, "shift": w.shift, "solver": w.solver, "seed": w.seed,
+        "full": res.full.astype(int).tolist(), "forced": res.forced.astype(int).tolist(),
+        "logit": _nan_to_none(res.logit), "nfe": int(res.nfe),
+        "features": [_nan_to_none(r) for r in res.features],
+        "sums": [_nan_to_none(r) for r in res.sums],
+        "stride": STRIDE,
+        "x_sample": [float(v) for v in x[::STRIDE]],
+        "dx_sample": [float(v) for v in dx[::STRIDE]],
+        "x_norm": float(np.linalg.norm(x)), "dx_norm": float(np.linalg.norm(dx)),
+    }
+    path = os.path.join(HERE, case + ".json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=0)
+    print(f"wrote {path}", flush=True)
+
+
+if __name__ == "__main__":
+    for c in sys.argv[1:] or list(CASES):
+        make(c)

@@ -11,6 +11,9 @@
 * Attention at the FLUX-2048 and Wan token counts on sampled query rows.
 """
 import dataclasses
+import importlib.util
+import json
+import os
 import time
 
 import numpy as np
@@ -66,6 +69,16 @@ def test_flux1024_two_blocks_each():
 # rounds to bf16 at the points where the oracle does, so the two differ only
 # where f32 and f64 accumulation round a value to neighbouring bf16 numbers.
 DX_TOL = 2e-2
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _golden_workload(case):
+    """The seeded workload of a stored case, as its generator defines it."""
+    spec = importlib.util.spec_from_file_location("make_full_size_goldens",
+                                                  os.path.join(GOLDEN, "make_full_size_goldens.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod.workload(case)
 
 
 def _golden_result(g):
@@ -78,27 +91,28 @@ def _golden_result(g):
                                  sums=f64(g["sums"]))
 
 
-def test_flux1024_full_depth_against_oracle_golden():
-    """FLUX-1024 at its full depth (19 double + 38 single blocks, full widths
-    and token counts) against the oracle's own gated run on T = 4, B = 2,
-    stored by tests/golden/make_flux1024_full_depth.py (the float64 oracle
-    needs about 40 minutes for it): decisions and logits by the margin
-    protocol, then the final latent and its displacement x_T - x_0 on every
-    256th element, and their norms."""
-    import json
-    import os
+@pytest.mark.parametrize("case", ["flux1024_full_depth"])
+def test_full_size_against_oracle_golden(case):
+    """Full-size runs against the oracle's own gated run, stored by
+    tests/golden/make_full_size_goldens.py (the float64 oracle needs 25-40
+    minutes for each): FLUX-1024 at its full depth (19 double + 38 single
+    blocks) on T = 4, B = 2, and the Wan block at its full 32760 video tokens
+    with UniPC on T = 3, B = 2.  Decisions and logits by the margin protocol,
+    then the final latent and its displacement x_T - x_0 on every 256th
+    element, and their norms."""
     torch = torch_cuda()
-    with open(os.path.join(os.path.dirname(__file__), "golden", "flux1024_full_depth.json")) as f:
+    with open(os.path.join(GOLDEN, case + ".json")) as f:
         g = json.load(f)
-    w = synth.reduced(synth.workload("flux1024"), T=g["T"], B=g["B"], name="flux1024_full_depth")
-    assert (w.model.n_double, w.model.n_single, w.shift, w.seed, w.solver) == \
-        (g["n_double"], g["n_single"], g["shift"], g["seed"], g["solver"])
+    w = _golden_workload(case)
+    m = w.model
+    assert (m.n_double, m.n_single, m.n_cross, m.n_img, w.T, w.B, w.shift, w.seed, w.solver) == \
+        (g["n_double"], g["n_single"], g["n_cross"], g["n_img"], g["T"], g["B"], g["shift"], g["seed"], g["solver"])
     t0 = time.time()
     weights, x0, text, gate = synth.make_inputs(w)
     x_gpu, sched, h = run_sampler(torch, w, weights, x0, text, gate, solver=w.solver)
     h.close()
     del weights
-    say(f"{w.name}: device schedule {sched.full.tolist()}, golden {g['full']} ({time.time() - t0:.1f} s)")
+    say(f"{case}: device schedule {sched.full.tolist()}, golden {g['full']} ({time.time() - t0:.1f} s)")
     ores = _golden_result(g)
     check_schedule_against_oracle(sched, ores)
     check_logits(sched, ores, gate)
@@ -110,7 +124,7 @@ def test_flux1024_full_depth_against_oracle_golden():
     dx = x - np.asarray(x0, np.float64).ravel()
     err = rel_l2(x[::k], g["x_sample"])
     err_dx = rel_l2(dx[::k], g["dx_sample"])
-    say(f"{w.name}: latent rel-L2 {err:.3e} (sampled), displacement rel-L2 {err_dx:.3e}, "
+    say(f"{case}: latent rel-L2 {err:.3e} (sampled), displacement rel-L2 {err_dx:.3e}, "
         f"norms {np.linalg.norm(x):.6e} / {g['x_norm']:.6e}, {np.linalg.norm(dx):.6e} / {g['dx_norm']:.6e}")
     assert err <= 2e-2
     assert abs(np.linalg.norm(x) - g["x_norm"]) <= 2e-2 * g["x_norm"]
