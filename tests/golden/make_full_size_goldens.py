@@ -15,7 +15,8 @@ stored rather than recomputed by the GPU tests.
 
 Stored per case: the schedule, the gate logits, forced flags, state features
 and indicator sums of every step, the final latent x_T and the displacement
-x_T - x_0 at every 256th element (values of each), and their full L2 norms.
+x_T - x_0 at every k-th element (k = 256 for FLUX, 2048 for Wan: about 1024
+values each), and their full L2 norms.
 Only the oracle and the seeded input generators are called.  Run from the
 repository root (no argument: every case):
     python tests/golden/make_full_size_goldens.py [case ...]
@@ -33,19 +34,18 @@ sys.path.insert(0, ROOT)
 from oracle import sample  # noqa: E402
 from paper_2608_09231_amd import synth  # noqa: E402
 
-STRIDE = 256
 HERE = os.path.dirname(os.path.abspath(__file__))
 
-# case -> (workload, reduction of synth.reduced)
+# case -> (workload, reduction of synth.reduced, sampling stride of the stored latents)
 CASES = {
-    "flux1024_full_depth": ("flux1024", dict(T=4, B=2)),
-    "wan14b_full_tokens": ("wan14b", dict(T=3, B=2, n_cross=1)),
+    "flux1024_full_depth": ("flux1024", dict(T=4, B=2), 256),
+    "wan14b_full_tokens": ("wan14b", dict(T=3, B=2, n_cross=1), 2048),
 }
 
 
 def workload(case):
     """The seeded workload of a case (shared with the GPU tests)."""
-    name, kw = CASES[case]
+    name, kw, _ = CASES[case]
     return synth.reduced(synth.workload(name), name=case, **kw)
 
 
@@ -64,6 +64,7 @@ def make(case):
     print(f"{case}: oracle done ({time.time() - t0:.0f} s): schedule {res.full.tolist()}", flush=True)
     x = np.asarray(res.x, np.float64).ravel()
     dx = x - np.asarray(x0, np.float64).ravel()
+    stride = CASES[case][2]
     out = {
         "note": f"oracle (float64) gated sample of {case}; written by tests/golden/make_full_size_goldens.py",
         "workload": CASES[case][0], "n_double": cfg.n_double, "n_single": cfg.n_single,
@@ -73,9 +74,9 @@ def make(case):
         "logit": _nan_to_none(res.logit), "nfe": int(res.nfe),
         "features": [_nan_to_none(r) for r in res.features],
         "sums": [_nan_to_none(r) for r in res.sums],
-        "stride": STRIDE,
-        "x_sample": [float(v) for v in x[::STRIDE]],
-        "dx_sample": [float(v) for v in dx[::STRIDE]],
+        "stride": stride,
+        "x_sample": [float(v) for v in x[::stride]],
+        "dx_sample": [float(v) for v in dx[::stride]],
         "x_norm": float(np.linalg.norm(x)), "dx_norm": float(np.linalg.norm(dx)),
     }
     path = os.path.join(HERE, case + ".json")

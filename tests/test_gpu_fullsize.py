@@ -91,15 +91,15 @@ def _golden_result(g):
                                  sums=f64(g["sums"]))
 
 
-@pytest.mark.parametrize("case", ["flux1024_full_depth"])
+@pytest.mark.parametrize("case", ["flux1024_full_depth", "wan14b_full_tokens"])
 def test_full_size_against_oracle_golden(case):
     """Full-size runs against the oracle's own gated run, stored by
     tests/golden/make_full_size_goldens.py (the float64 oracle needs 25-40
     minutes for each): FLUX-1024 at its full depth (19 double + 38 single
     blocks) on T = 4, B = 2, and the Wan block at its full 32760 video tokens
     with UniPC on T = 3, B = 2.  Decisions and logits by the margin protocol,
-    then the final latent and its displacement x_T - x_0 on every 256th
-    element, and their norms."""
+    then the final latent and its displacement x_T - x_0 on the stored
+    elements (every 256th, every 2048th for Wan), and their norms."""
     torch = torch_cuda()
     with open(os.path.join(GOLDEN, case + ".json")) as f:
         g = json.load(f)
