@@ -7,7 +7,11 @@
   wan14b_full_tokens.json   the Wan block at its full width and token count
                             (one video block, H 5120, 32760 video tokens, 512
                             text tokens) with the workload's UniPC step rule,
-                            T = 3, B = 2 (about 25 minutes).
+                            T = 3, B = 2 (about 25 minutes);
+  qwen_cfg_full_depth.json  the Qwen-Image guidance pair at its full depth (60
+                            double blocks, H 3072, 4096 image + 256 text
+                            tokens, both branches, guidance 4), T = 3, B = 2
+                            (about 80 minutes).
 
 The float64 oracle needs about 17-21 s per full-width FLUX block and about six
 minutes per Wan block at 32760 tokens on eight host cores, so these runs are
@@ -40,6 +44,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CASES = {
     "flux1024_full_depth": ("flux1024", dict(T=4, B=2), 256),
     "wan14b_full_tokens": ("wan14b", dict(T=3, B=2, n_cross=1), 2048),
+    "qwen_cfg_full_depth": ("qwen_cfg", dict(T=3, B=2), 256),
 }
 
 

@@ -68,7 +68,14 @@ def test_flux1024_two_blocks_each():
 # The displacement x_T - x_0 is held to the latents' own bar: the device
 # rounds to bf16 at the points where the oracle does, so the two differ only
 # where f32 and f64 accumulation round a value to neighbouring bf16 numbers.
+# Through a deep stack, and most under guidance (v = v_u + g (v_c - v_u)
+# scales the branches' differences by g), such rounding differences grow:
+# the bar is the larger of 2e-2 and twice the device's own spread between a
+# run from x_0 and one from x_0 perturbed at f32 rounding level (relative
+# 1e-7), which the test measures each time.
 DX_TOL = 2e-2
+NOISE_FACTOR = 2.0
+NOISE_REL = 1e-7
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
@@ -91,15 +98,18 @@ def _golden_result(g):
                                  sums=f64(g["sums"]))
 
 
-@pytest.mark.parametrize("case", ["flux1024_full_depth", "wan14b_full_tokens"])
+@pytest.mark.parametrize("case", ["flux1024_full_depth", "wan14b_full_tokens", "qwen_cfg_full_depth"])
 def test_full_size_against_oracle_golden(case):
     """Full-size runs against the oracle's own gated run, stored by
-    tests/golden/make_full_size_goldens.py (the float64 oracle needs 25-40
+    tests/golden/make_full_size_goldens.py (the float64 oracle needs 25-80
     minutes for each): FLUX-1024 at its full depth (19 double + 38 single
-    blocks) on T = 4, B = 2, and the Wan block at its full 32760 video tokens
-    with UniPC on T = 3, B = 2.  Decisions and logits by the margin protocol,
-    then the final latent and its displacement x_T - x_0 on the stored
-    elements (every 256th, every 2048th for Wan), and their norms."""
+    blocks) on T = 4, B = 2, the Wan block at its full 32760 video tokens
+    with UniPC on T = 3, B = 2, and the Qwen-Image guidance pair at its full
+    depth (60 double blocks, g = 4) on T = 3, B = 2.  Decisions and logits by
+    the margin protocol, then the final latent and its displacement x_T - x_0
+    on the stored elements (every 256th, every 2048th for Wan), and their
+    norms, against the larger of 2e-2 and twice the rounding-noise spread of
+    the device's own runs (see NOISE_FACTOR)."""
     torch = torch_cuda()
     with open(os.path.join(GOLDEN, case + ".json")) as f:
         g = json.load(f)
@@ -110,9 +120,15 @@ def test_full_size_against_oracle_golden(case):
     t0 = time.time()
     weights, x0, text, gate = synth.make_inputs(w)
     x_gpu, sched, h = run_sampler(torch, w, weights, x0, text, gate, solver=w.solver)
+    # the same sample from x_0 perturbed at f32 rounding level: the spread the
+    # problem itself gives to rounding differences
+    rng = np.random.default_rng(0)
+    xp0 = (x0.astype(np.float64) * (1.0 + NOISE_REL * rng.standard_normal(x0.shape))).astype(np.float32)
+    x_pert, sched_p, h = run_sampler(torch, w, weights, xp0, text, gate, solver=w.solver, handle=h)
     h.close()
     del weights
     say(f"{case}: device schedule {sched.full.tolist()}, golden {g['full']} ({time.time() - t0:.1f} s)")
+    assert (sched_p.full == sched.full).all()
     ores = _golden_result(g)
     check_schedule_against_oracle(sched, ores)
     check_logits(sched, ores, gate)
@@ -122,13 +138,17 @@ def test_full_size_against_oracle_golden(case):
     k = int(g["stride"])
     x = x_gpu.ravel()
     dx = x - np.asarray(x0, np.float64).ravel()
+    floor = rel_l2(x_pert.ravel(), x)
+    floor_dx = rel_l2(x_pert.ravel() - xp0.astype(np.float64).ravel(), dx)
+    tol, tol_dx = max(2e-2, NOISE_FACTOR * floor), max(DX_TOL, NOISE_FACTOR * floor_dx)
     err = rel_l2(x[::k], g["x_sample"])
     err_dx = rel_l2(dx[::k], g["dx_sample"])
-    say(f"{case}: latent rel-L2 {err:.3e} (sampled), displacement rel-L2 {err_dx:.3e}, "
+    say(f"{case}: latent rel-L2 {err:.3e} (sampled; device rounding spread {floor:.3e}, bound {tol:.3e}), "
+        f"displacement rel-L2 {err_dx:.3e} (spread {floor_dx:.3e}, bound {tol_dx:.3e}), "
         f"norms {np.linalg.norm(x):.6e} / {g['x_norm']:.6e}, {np.linalg.norm(dx):.6e} / {g['dx_norm']:.6e}")
-    assert err <= 2e-2
+    assert err <= tol
     assert abs(np.linalg.norm(x) - g["x_norm"]) <= 2e-2 * g["x_norm"]
-    assert err_dx <= DX_TOL
+    assert err_dx <= tol_dx
     assert abs(np.linalg.norm(dx) - g["dx_norm"]) <= DX_TOL * g["dx_norm"]
 
 
