@@ -499,7 +499,7 @@ dit_status ensure_lanes(dit_cache* c, int S) {
 
 dit_status alloc_workspace(dit_cache* c) {
   const size_t e = c->esz;
-  const int H = c->H, N = c->N, Nt = c->Nt;
+  const int H = c->H, N = c->N;
   TRY(dalloc(c, &c->xs, (size_t)N * c->C * e));
   TRY(dalloc(c, &c->yf, (size_t)N * H * e));
   TRY(dalloc(c, &c->vel, (size_t)c->nb * N * c->C * 4));
